@@ -1,0 +1,189 @@
+#!/usr/bin/env python3
+"""SLORR-Hoyer forward + backward throughput on one MI355X.
+
+A step is one pass of the whole hot path over the ViT-B/16-shaped weight set
+(48 bf16 matrices: 12 blocks of qkv 2304x768, proj 768x768, fc1 3072x768,
+fc2 768x3072): Frobenius norms, normalisation, T = 6 Polar Express steps
+(3 MFMA GEMMs each), trace, values and gradients of every matrix, replayed
+as one hipGraph on the current stream. Inputs are resident in HBM before the
+timed region starts.
+
+Prints one JSON line: throughput in weight-sets/s, the roofline of the
+dominant kernel (live HIP-event timing of each launch on the stream it runs
+on) and the CPU oracle's rate on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA: fp16/bf16 operands, fp32 operands
+GEMM_OPS = ("gram", "poly", "update", "last")
+
+
+def _alg_flops_per_launch(shapes, op):
+    """Paper count (Sec. 3): per step 2 P^2 Q (A = X X^T) + 2 P^3 (A A) + 2 P^2 Q (B X)."""
+    tot = 0.0
+    for m, n in shapes:
+        if m == 0 or n == 0:
+            continue
+        P, Q = min(m, n), max(m, n)
+        tot += 2.0 * P ** 3 if op == "poly" else 2.0 * P * P * Q
+    return tot
+
+
+def _kernels_hash():
+    with open(os.path.join(ROOT, "paper_2607_08754_amd", "csrc", "kernels.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _traffic(config, op):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{config}.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernels_sha256_16") != _kernels_hash():
+        return None
+    entry = t.get("per_launch_bytes", {}).get(op)
+    return float(entry) if entry is not None else None
+
+
+def cpu_baseline(cfg, arrs, gpu_vals, gpu_grads, seconds):
+    """The oracle, as it stands, on whole blocks of the set until `seconds`
+    of CPU work; also compares the sampled matrices with the timed GPU output."""
+    import numpy as np
+    from oracle.pe_schedule import pe_schedule
+    from oracle.slorr import fwd_bwd
+    from workloads import widen
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    table = pe_schedule(cfg.iters)
+    per_block = 4 if cfg.name.startswith("vit") else 1
+    nblocks = cfg.n // per_block
+    done, worst_v, worst_g = 0, 0.0, 0.0
+    t0 = time.perf_counter()
+    while done < nblocks and (time.perf_counter() - t0) < seconds:
+        for i in range(done * per_block, (done + 1) * per_block):
+            W = widen(arrs[i], cfg.dtype)
+            r = fwd_bwd(W, "hoyer", table)
+            worst_v = max(worst_v, abs(gpu_vals[i] - r.value) / abs(r.value))
+            s1 = 2.0 * r.n_hat / r.f_eps ** 2
+            den = max(np.linalg.norm(r.grad), np.linalg.norm(s1 * r.polar))
+            worst_g = max(worst_g, float(np.linalg.norm(gpu_grads[i] - r.grad) / den))
+        done += 1
+    el = time.perf_counter() - t0
+    frac = done * per_block / cfg.n
+    return {"value": frac / el, "unit": "weight-sets/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{done} of {nblocks} blocks ({done * per_block} of {cfg.n} matrices), "
+                      f"NumPy float64, {el:.1f} s",
+            "parity_on_sample": {"max_value_rel_err": worst_v, "max_grad_rel_err": worst_g}}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="vit_b16")
+    ap.add_argument("--kind", default="hoyer", choices=["hoyer", "nuclear"])
+    ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the hot path has no "
+              "cross-GPU step to time.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_08754_amd import Plan
+    from workloads import CONFIGS, make_set
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    t_gen = time.perf_counter()
+    arrs = make_set(cfg.name, 0)
+    W = []
+    for a in arrs:
+        t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if cfg.dtype == "bf16" else torch.from_numpy(a)
+        W.append(t.to(dev))
+    G = [torch.empty(a.shape, dtype=torch.float32, device=dev) for a in arrs]
+    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, device=dev)
+    info = plan.info()
+    print(f"[bench] {cfg.name}: {cfg.n} matrices, inputs ready in {time.perf_counter() - t_gen:.1f} s, "
+          f"{info['launches']} launches per step", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(args.warmup):
+        vals = plan(W, G)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(args.steps):
+        vals = plan(W, G)
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    gpu_vals = vals.cpu().numpy().astype(np.float64)
+    print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
+
+    # per-launch durations, HIP events on the launch stream
+    per_op = {}
+    for _ in range(args.profile_steps):
+        _, launches = plan.profiled(W, G)
+        for op, t in launches:
+            per_op.setdefault(op, []).append(t)
+    torch.cuda.synchronize()
+    gpu_grads = [g.cpu().numpy().astype(np.float64) for g in G]
+    op_ms = {op: {"launches_per_step": len(v) // args.profile_steps, "avg_ms": float(np.mean(v)),
+                  "ms_per_step": float(np.sum(v)) / args.profile_steps} for op, v in per_op.items()}
+    dominant = max((op for op in op_ms if op in GEMM_OPS), key=lambda o: op_ms[o]["ms_per_step"])
+    flops = _alg_flops_per_launch(cfg.shapes, dominant)
+    avg_s = op_ms[dominant]["avg_ms"] * 1e-3
+    achieved = flops / avg_s / 1e12
+    peak = PEAK_TFLOPS[cfg.dtype]
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4), "traffic": _traffic(cfg.name, dominant),
+                "kernel": f"k_gemm<{dominant}>", "alg_flops_per_launch": flops,
+                "avg_launch_ms": op_ms[dominant]["avg_ms"]}
+
+    value = 1000.0 / ms
+    chain_ms = sum(op_ms[o]["ms_per_step"] for o in op_ms if o in GEMM_OPS)
+    out = {
+        "metric": "SLORR-Hoyer fwd+bwd weight-sets/s (ViT-B/16 shapes); % of MFMA peak",
+        "value": round(value, 3), "unit": "weight-sets/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f16" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.n} matrices ({cfg.note}), "
+                               f"{cfg.dtype} weights, T={cfg.iters}, {args.kind}",
+                   "matrices": cfg.n, "iters": cfg.iters, "kind": args.kind},
+        "roofline": roofline,
+        "matrices_per_s": round(cfg.n * value, 1),
+        "paper_tflops_effective": round(cfg.flops() / (ms * 1e-3) / 1e12, 2),
+        "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
+        "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, arrs, gpu_vals, gpu_grads, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,207 @@
+/*
+ * slorr.h -- C ABI of the SLORR regularizer hot path on MI355X (gfx950).
+ *
+ * SLORR (Sec. 3 of the paper) adds to the training loss, for every regularized
+ * weight matrix W (M x N, row-major), one of two spectral penalties:
+ *
+ *   SLORR-Hoyer  L = ||W||_*^2 / ||W||_F^2   (squared l1/l2 ratio of the
+ *                                             singular values)
+ *   SLORR-Nuc    L = ||W||_*                 (nuclear norm)
+ *
+ * with gradients (Eq. SLORR_grads, the minimum-norm Clarke gradients of App. A)
+ *
+ *   Hoyer  dL/dW = 2 (n/f) (P/f - n/f^3 W),   Nuc  dL/dW = P
+ *
+ * where P stands for the polar factor U V^T, n for ||W||_* and f for ||W||_F.
+ * No SVD is formed: P is approximated by T Polar Express steps on
+ * X_0 = W / (||W||_F + eps) (Sec. 3 "Computing the polar factor"; App. E.1),
+ *
+ *   A = X X^T,  B = b_t A + c_t A A,  X <- a_t X + B X        t = 1..T,
+ *
+ * n by the trace sum(W * P) (Sec. 3 "Computing the nuclear and Frobenius
+ * norms"), and f by sqrt(sum W^2); every f in the value and gradient is
+ * replaced by f + eps as in Listing 1. Gradients are not propagated through
+ * the iteration (Sec. 3 "Combining everything").
+ *
+ * The products are formed on the short side of W: P = min(M, N), Q = max(M, N),
+ * W is used as is when M <= N and transposed when M > N (the orientation of the
+ * cost 4 P^2 Q + 2 P^3 per step, Sec. 3 "Computational cost").
+ *
+ * Execution model
+ *   - The caller owns every device buffer (weights, gradients, values and the
+ *     workspace). The library allocates no device memory.
+ *   - Work is enqueued asynchronously on the caller's HIP stream. Validation is
+ *     complete before anything is enqueued: a non-OK status means nothing was
+ *     enqueued. Device faults surface on a later HIP call as SLORR_ERR_HIP.
+ *   - A plan may be used by one thread and one stream at a time; calls on one
+ *     plan are ordered by the stream they are enqueued on.
+ *   - No C++ exception crosses this interface.
+ *   - The library does no numeric caching between calls (SLORR is stateless,
+ *     Sec. 2): every call recomputes from the current weights.
+ */
+#ifndef SLORR_H
+#define SLORR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__) || defined(__clang__)
+#define SLORR_API __attribute__((visibility("default")))
+#else
+#define SLORR_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SLORR_OK = 0,
+  SLORR_ERR_INVALID_ARGUMENT = 1, /* null pointer, bad size, misaligned pointer, aliasing */
+  SLORR_ERR_UNSUPPORTED = 2,      /* unknown dtype/kind/degree, size beyond the limits   */
+  SLORR_ERR_PLAN_MISMATCH = 3,    /* call arguments disagree with the plan               */
+  SLORR_ERR_WORKSPACE = 4,        /* workspace missing, too small or misaligned          */
+  SLORR_ERR_HIP = 5,              /* a HIP runtime call failed                            */
+  SLORR_ERR_INTERNAL = 6          /* unexpected internal failure                          */
+} slorr_status_t;
+
+/* Which regularizer (Sec. 3, definitions of L_hoyer and L_nuc). */
+typedef enum { SLORR_HOYER = 0, SLORR_NUCLEAR = 1 } slorr_kind_t;
+
+/* Storage type of the weights. F32: the iteration runs in fp32 (fp32 MFMA).
+ * BF16: the iteration runs on fp16 MFMA operands with power-of-two scaling and
+ * fp32 accumulation; norms and traces are accumulated in fp32 or wider. */
+typedef enum { SLORR_F32 = 0, SLORR_BF16 = 1 } slorr_dtype_t;
+
+/* Shape of one weight matrix: row-major, contiguous, rows x cols.
+ * A conv kernel (C_out, C_in, k_h, k_w) is passed as (C_out, C_in*k_h*k_w)
+ * (App. C.1). rows, cols >= 0; min(rows, cols) <= 16384 and
+ * max(rows, cols) <= 1048576 (SLORR_ERR_UNSUPPORTED otherwise). A matrix with
+ * rows == 0 or cols == 0 has value 0 and no gradient elements. */
+typedef struct { int32_t rows, cols; } slorr_shape_t;
+
+/* Flags for slorr_options_t.flags */
+#define SLORR_ACCUMULATE  0x1u  /* out_grads[i] += result (App. E.3, W.grad += lambda G) */
+#define SLORR_VALUES_ONLY 0x2u  /* values only: no gradient is written, out_grads may be NULL */
+#define SLORR_NO_GRAPH    0x4u  /* enqueue kernels one by one instead of replaying a hipGraph */
+#define SLORR_AUX         0x8u  /* out_vals also receives n_hat_i and f_i (see below) */
+
+typedef struct {
+  int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */
+  int32_t degree;        /* 5 (quintic, the paper's setting) or 3 (cubic, c_t = 0); 0 -> 5   */
+  double ell;            /* lower bound l in (0, 1) on normalised singular values; 0 -> 1e-3 */
+  const double *coeffs;  /* optional host array [iters][3] of (a_t, b_t, c_t); NULL -> the
+                            library's greedy minimax schedule for (ell, degree). Copied at
+                            plan creation. */
+  float eps;             /* added to ||W||_F (Listing 1); >= 0 and finite                    */
+  uint32_t flags;        /* SLORR_* flags above                                              */
+} slorr_options_t;
+
+typedef struct slorr_plan_s *slorr_plan_t;
+
+/* Fill *opts with the defaults: iters 6, degree 5, ell 1e-3, coeffs NULL,
+ * eps 0, flags 0. */
+SLORR_API void slorr_default_options(slorr_options_t *opts);
+
+/* Greedy Polar Express schedule (Sec. 3; App. E.1), host only, no device use.
+ * Step t minimises max |1 - p_t(x)| over [l_t, u_t] among odd polynomials of
+ * the given degree, starting from [ell, 1]; the next interval is
+ * [1 - E_t, 1 + E_t] with E_t the optimal error. Once E_t < 1e-4 (the next
+ * minimax problem is below double-precision resolution) every later step uses
+ * the limit polynomial of the recursion, Newton-Schulz: (15x - 10x^3 + 3x^5)/8
+ * for degree 5, (3x - x^3)/2 for degree 3. Writes iters rows (a_t, b_t, c_t)
+ * to out (host array of 3*iters doubles; c_t = 0 for degree 3). */
+SLORR_API slorr_status_t slorr_pe_coefficients(double ell, int32_t degree, int32_t iters, double *out);
+
+/* Build a plan for a fixed set of n matrices (host only, no device use).
+ * shapes: host array of n shapes. n >= 0 (n == 0 is a valid empty set).
+ * opts may be NULL (defaults). *workspace_bytes receives the size of the
+ * device workspace the plan needs (never 0). On error *plan is set to NULL. */
+SLORR_API slorr_status_t slorr_plan_create(slorr_plan_t *plan, int32_t n, const slorr_shape_t *shapes,
+                                 slorr_dtype_t dtype, slorr_kind_t kind,
+                                 const slorr_options_t *opts, size_t *workspace_bytes);
+
+/* Attach caller-owned device memory as the plan's workspace. dev_ptr must be
+ * 256-byte aligned and at least the size slorr_plan_create reported. The
+ * library writes its static tables into it (synchronous host-to-device copy on
+ * the current device) and keeps the pointer until the next call to this
+ * function or slorr_plan_destroy; the caller keeps the memory alive that long.
+ * The current device at this call is the plan's device. */
+SLORR_API slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t bytes);
+
+/* Forward + backward of the regularizer over the whole set.
+ *   n, shapes, kind, iters : must equal the plan's (SLORR_ERR_PLAN_MISMATCH)
+ *   weights   : host array of n device pointers, weights[i] -> rows_i x cols_i
+ *               row-major contiguous values of the plan's dtype, 16-byte aligned
+ *               (NULL allowed only for empty matrices)
+ *   out_vals  : device float array. Receives L_0..L_{n-1} then sum_i L_i (index
+ *               order) at out_vals[n]. With SLORR_AUX, also n_hat_i at
+ *               out_vals[n+1+i] and ||W_i||_F at out_vals[2n+1+i]. 4-byte aligned.
+ *   out_grads : host array of n device pointers to fp32 rows_i x cols_i row-major
+ *               buffers, 16-byte aligned, receiving grad_scale * dL_i/dW_i
+ *               (or adding it with SLORR_ACCUMULATE). Must not overlap the
+ *               weights or each other. May be NULL with SLORR_VALUES_ONLY.
+ *   grad_scale: upstream factor g (e.g. lambda times the upstream gradient).
+ *   stream    : hipStream_t to enqueue on (NULL = the null stream).
+ * A matrix whose ||W||_F + eps is 0 gets value 0 and gradient 0; NaN or Inf in
+ * a matrix propagate to that matrix's outputs and to the sum only. */
+SLORR_API slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const *weights,
+                                 const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                                 float *out_vals, float *const *out_grads, float grad_scale,
+                                 void *stream);
+
+/* Kernel kinds of the launch schedule, as reported by slorr_reg_fwd_bwd_profiled. */
+typedef enum {
+  SLORR_OP_SUMSQ = 0,     /* partial sums of W^2 per chunk               */
+  SLORR_OP_NORM = 1,      /* ||W||_F and ||W||_F + eps per matrix         */
+  SLORR_OP_PREP = 2,      /* X_0 = W / (||W||_F + eps), short-side layout */
+  SLORR_OP_GRAM = 3,      /* A = X X^T                                    */
+  SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
+  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X                              */
+  SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
+  SLORR_OP_FINALIZE = 7,  /* values, set sum, gradient factors            */
+  SLORR_OP_GRAD = 8       /* gradient epilogue                            */
+} slorr_op_t;
+
+/* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the
+ * schedule is enqueued launch by launch (no graph) with a HIP event recorded
+ * before and after every launch on `stream`; the call then synchronises that
+ * stream and writes each launch's duration in milliseconds to launch_ms and
+ * its kind to launch_op (host arrays of slorr_plan_info_t.launches entries;
+ * launch_op may be NULL). Not meant for training loops: it blocks the host. */
+SLORR_API slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
+                                 const void *const *weights, const slorr_shape_t *shapes,
+                                 slorr_kind_t kind, int32_t iters, float *out_vals,
+                                 float *const *out_grads, float grad_scale, void *stream,
+                                 float *launch_ms, int32_t *launch_op);
+
+/* Release the plan (and its captured graph). Does not free the workspace.
+ * Synchronises with work the plan has enqueued. NULL is accepted. */
+SLORR_API slorr_status_t slorr_plan_destroy(slorr_plan_t plan);
+
+/* Plan facts for callers and benchmarks. */
+typedef struct {
+  int32_t n;               /* matrices in the plan                                  */
+  int32_t groups;          /* distinct canonical (P, Q) shapes                       */
+  int32_t iters;           /* T                                                      */
+  int32_t launches;        /* kernels per call                                       */
+  int64_t gemm_tiles;      /* output tiles over all GEMM launches of one call        */
+  double paper_flops;      /* T * sum_i (4 P_i^2 Q_i + 2 P_i^3) (Sec. 3)             */
+  double mfma_flops;       /* flops the MFMA units execute per call (padded tiles)   */
+  double weight_bytes;     /* sum_i rows_i * cols_i * sizeof(dtype)                  */
+  size_t workspace_bytes;
+} slorr_plan_info_t;
+
+SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info);
+
+/* Name of a status code (static string). */
+SLORR_API const char *slorr_status_string(slorr_status_t status);
+
+/* Detail message of the last failing call on this thread ("" if none). */
+SLORR_API const char *slorr_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLORR_H */

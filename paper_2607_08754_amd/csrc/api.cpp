@@ -1,0 +1,382 @@
+// C ABI of the SLORR library: validation, workspace tables, per-call pointer
+// table, hipGraph capture and replay. See include/slorr.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <new>
+#include <stdexcept>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "kernels.hpp"
+#include "plan.hpp"
+#include "slorr.h"
+
+struct slorr_plan_s {
+  slorr::Plan p;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+slorr_status_t fail(slorr_status_t s, const std::string &msg) {
+  g_last_error = msg;
+  return s;
+}
+
+struct ApiError {
+  slorr_status_t status;
+  std::string msg;
+};
+
+void hip_check(hipError_t e, const char *what) {
+  if (e != hipSuccess) throw ApiError{SLORR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e)};
+}
+
+template <typename F>
+slorr_status_t guarded(F &&f) {
+  try {
+    g_last_error.clear();
+    return f();
+  } catch (const ApiError &e) {
+    return fail(e.status, e.msg);
+  } catch (const slorr::HipError &e) {
+    return fail(SLORR_ERR_HIP, e.what());
+  } catch (const std::invalid_argument &e) {
+    return fail(SLORR_ERR_INVALID_ARGUMENT, e.what());
+  } catch (const std::domain_error &e) {
+    return fail(SLORR_ERR_UNSUPPORTED, e.what());
+  } catch (const std::bad_alloc &) {
+    return fail(SLORR_ERR_INTERNAL, "host allocation failed");
+  } catch (const std::exception &e) {
+    return fail(SLORR_ERR_INTERNAL, e.what());
+  } catch (...) {
+    return fail(SLORR_ERR_INTERNAL, "unknown exception");
+  }
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+void release_runtime(slorr::Plan &p) {
+  if (p.device >= 0) {
+    (void)hipSetDevice(p.device);
+    (void)hipDeviceSynchronize();
+  }
+  if (p.graph_exec) (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(p.graph_exec));
+  if (p.graph) (void)hipGraphDestroy(static_cast<hipGraph_t>(p.graph));
+  p.graph_exec = p.graph = nullptr;
+  if (p.capture_stream) (void)hipStreamDestroy(static_cast<hipStream_t>(p.capture_stream));
+  p.capture_stream = nullptr;
+  for (int k = 0; k < 2; ++k) {
+    if (p.staging_event[k]) (void)hipEventDestroy(static_cast<hipEvent_t>(p.staging_event[k]));
+    if (p.staging[k]) (void)hipHostFree(p.staging[k]);
+    p.staging_event[k] = p.staging[k] = nullptr;
+  }
+  p.dyn_valid = false;
+}
+
+// Validates a call against the plan and uploads the per-call pointer table
+// (only when it changed). Returns the plan; nothing is enqueued on failure
+// except when the table upload itself fails.
+slorr::Plan &prepare_call(slorr_plan_t plan, int32_t n, const void *const *weights,
+                          const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                          float *out_vals, float *const *out_grads, float grad_scale,
+                          hipStream_t s) {
+    if (!plan) throw std::invalid_argument("plan is NULL");
+    slorr::Plan &p = plan->p;
+    if (n != p.n) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "n differs from the plan"};
+    if (kind != p.kind) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "kind differs from the plan"};
+    if (iters != p.iters) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "iters differs from the plan"};
+    if (n > 0 && !shapes) throw std::invalid_argument("shapes is NULL");
+    for (int i = 0; i < n; ++i)
+      if (shapes[i].rows != p.shapes[i].rows || shapes[i].cols != p.shapes[i].cols)
+        throw ApiError{SLORR_ERR_PLAN_MISMATCH, "shape of matrix " + std::to_string(i) + " differs from the plan"};
+    if (!out_vals) throw std::invalid_argument("out_vals is NULL");
+    if (!aligned(out_vals, 4)) throw std::invalid_argument("out_vals must be 4-byte aligned");
+    const bool want_grad = !(p.flags & SLORR_VALUES_ONLY);
+    if (n > 0 && !weights) throw std::invalid_argument("weights is NULL");
+    if (want_grad && n > 0 && !out_grads) throw std::invalid_argument("out_grads is NULL");
+    // pointer checks and overlap of written ranges
+    std::vector<std::pair<uintptr_t, std::pair<uintptr_t, int>>> spans;  // begin, (end, is_grad)
+    for (int i = 0; i < n; ++i) {
+      const slorr::MatDesc &d = p.mats[i];
+      if (d.empty) continue;
+      const size_t elems = size_t(d.rows) * d.cols;
+      if (!weights[i]) throw std::invalid_argument("weights[" + std::to_string(i) + "] is NULL");
+      if (!aligned(weights[i], 16)) throw std::invalid_argument("weights[" + std::to_string(i) + "] must be 16-byte aligned");
+      const uintptr_t wb = reinterpret_cast<uintptr_t>(weights[i]);
+      spans.push_back({wb, {wb + elems * p.elem_bytes(), 0}});
+      if (want_grad) {
+        if (!out_grads[i]) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] is NULL");
+        if (!aligned(out_grads[i], 16)) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] must be 16-byte aligned");
+        const uintptr_t gb = reinterpret_cast<uintptr_t>(out_grads[i]);
+        spans.push_back({gb, {gb + elems * sizeof(float), 1}});
+      }
+    }
+    std::sort(spans.begin(), spans.end());
+    uintptr_t reach_all = 0, reach_grad = 0;   // furthest end of earlier spans / grad spans
+    for (const auto &s : spans) {
+      const bool is_grad = s.second.second != 0;
+      if (s.first < reach_grad || (is_grad && s.first < reach_all))
+        throw std::invalid_argument("out_grads overlap the weights or each other");
+      reach_all = std::max(reach_all, s.second.first);
+      if (is_grad) reach_grad = std::max(reach_grad, s.second.first);
+    }
+    if (!p.ws) throw ApiError{SLORR_ERR_WORKSPACE, "no workspace attached to the plan"};
+    int dev = -1;
+    hip_check(hipGetDevice(&dev), "hipGetDevice");
+    if (dev != p.device) throw std::invalid_argument("current device differs from the workspace's device");
+
+    // per-call pointer table: upload only when it changed
+    std::vector<slorr::DynDesc> dyn(n);
+    for (int i = 0; i < n; ++i) {
+      dyn[i].w = p.mats[i].empty ? nullptr : weights[i];
+      dyn[i].g = (want_grad && !p.mats[i].empty) ? out_grads[i] : nullptr;
+    }
+    slorr::CallParams call{};
+    call.out_vals = out_vals;
+    call.grad_scale = grad_scale;
+    const bool same = p.dyn_valid && p.call_cache.out_vals == call.out_vals &&
+                      p.call_cache.grad_scale == call.grad_scale &&
+                      std::memcmp(p.dyn_cache.data(), dyn.data(), n * sizeof(slorr::DynDesc)) == 0;
+    if (!same) {
+      const int k = p.staging_next;
+      p.staging_next ^= 1;
+      hipEvent_t ev = static_cast<hipEvent_t>(p.staging_event[k]);
+      hip_check(hipEventSynchronize(ev), "hipEventSynchronize");
+      char *st = static_cast<char *>(p.staging[k]);
+      std::memset(st, 0, p.dyn_bytes());
+      if (n) std::memcpy(st, dyn.data(), n * sizeof(slorr::DynDesc));
+      std::memcpy(st + (p.off_call - p.off_dyn), &call, sizeof(call));
+      hip_check(hipMemcpyAsync(static_cast<char *>(p.ws) + p.off_dyn, st, p.dyn_bytes(),
+                               hipMemcpyHostToDevice, s),
+                "hipMemcpyAsync pointer table");
+      hip_check(hipEventRecord(ev, s), "hipEventRecord");
+      p.dyn_cache = dyn;
+      p.call_cache = call;
+      p.dyn_valid = true;
+    }
+
+    return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+void slorr_default_options(slorr_options_t *o) {
+  if (!o) return;
+  o->iters = 6;
+  o->degree = 5;
+  o->ell = 1e-3;
+  o->coeffs = nullptr;
+  o->eps = 0.0f;
+  o->flags = 0;
+}
+
+slorr_status_t slorr_pe_coefficients(double ell, int32_t degree, int32_t iters, double *out) {
+  return guarded([&]() -> slorr_status_t {
+    if (!out) throw std::invalid_argument("out is NULL");
+    if (iters < 1 || iters > 1000) throw std::invalid_argument("iters must be in [1, 1000]");
+    if (degree != 3 && degree != 5) throw std::domain_error("degree must be 3 or 5");
+    if (!(ell > 0.0 && ell < 1.0)) throw std::invalid_argument("ell must be in (0, 1)");
+    slorr::greedy_schedule(ell, degree, iters, out);
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_plan_create(slorr_plan_t *plan, int32_t n, const slorr_shape_t *shapes,
+                                 slorr_dtype_t dtype, slorr_kind_t kind,
+                                 const slorr_options_t *opts, size_t *workspace_bytes) {
+  if (plan) *plan = nullptr;
+  return guarded([&]() -> slorr_status_t {
+    if (!plan) throw std::invalid_argument("plan is NULL");
+    if (!workspace_bytes) throw std::invalid_argument("workspace_bytes is NULL");
+    if (n < 0) throw std::invalid_argument("n must be >= 0");
+    if (n > 0 && !shapes) throw std::invalid_argument("shapes is NULL");
+    slorr_options_t o;
+    slorr_default_options(&o);
+    if (opts) o = *opts;
+    auto *h = new slorr_plan_s();
+    try {
+      slorr::Plan &p = h->p;
+      p.n = n;
+      p.dtype = dtype;
+      p.kind = kind;
+      p.iters = o.iters == 0 ? 6 : o.iters;
+      p.degree = o.degree == 0 ? 5 : o.degree;
+      p.ell = o.ell == 0.0 ? 1e-3 : o.ell;
+      p.eps = o.eps;
+      p.flags = o.flags;
+      p.shapes.assign(shapes, shapes + n);
+      if (o.coeffs) {
+        if (p.iters < 1 || p.iters > 1000) throw std::invalid_argument("iters must be in [1, 1000]");
+        p.coeffs.assign(o.coeffs, o.coeffs + size_t(p.iters) * 3);
+      }
+      slorr::build_plan(p);
+      *workspace_bytes = p.ws_bytes;
+    } catch (...) {
+      delete h;
+      throw;
+    }
+    *plan = h;
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
+  return guarded([&]() -> slorr_status_t {
+    if (!plan || !info) throw std::invalid_argument("NULL argument");
+    const slorr::Plan &p = plan->p;
+    info->n = p.n;
+    info->groups = p.groups;
+    info->iters = p.iters;
+    info->launches = int32_t(p.launches.size());
+    int64_t tiles = 0;
+    for (const auto &l : p.launches)
+      if (l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Update ||
+          l.op == slorr::Op::Last)
+        tiles += l.grid;
+    info->gemm_tiles = tiles;
+    info->paper_flops = p.paper_flops;
+    info->mfma_flops = p.mfma_flops;
+    info->weight_bytes = p.weight_bytes;
+    info->workspace_bytes = p.ws_bytes;
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t bytes) {
+  return guarded([&]() -> slorr_status_t {
+    if (!plan) throw std::invalid_argument("plan is NULL");
+    slorr::Plan &p = plan->p;
+    if (!dev_ptr) throw ApiError{SLORR_ERR_WORKSPACE, "workspace pointer is NULL"};
+    if (!aligned(dev_ptr, 256)) throw ApiError{SLORR_ERR_WORKSPACE, "workspace must be 256-byte aligned"};
+    if (bytes < p.ws_bytes)
+      throw ApiError{SLORR_ERR_WORKSPACE, "workspace too small: need " + std::to_string(p.ws_bytes) +
+                                              " bytes, got " + std::to_string(bytes)};
+    release_runtime(p);
+    p.ws = nullptr;
+    int dev = -1;
+    hip_check(hipGetDevice(&dev), "hipGetDevice");
+    // static tables, one synchronous copy
+    std::vector<char> host(p.off_static_end, 0);
+    auto put = [&](size_t off, const void *src, size_t n) {
+      if (n) std::memcpy(host.data() + off, src, n);
+    };
+    put(p.off_mats, p.mats.data(), p.mats.size() * sizeof(slorr::MatDesc));
+    put(p.off_tiles_pp, p.tiles_pp.data(), p.tiles_pp.size() * sizeof(slorr::Tile));
+    put(p.off_tiles_pq, p.tiles_pq.data(), p.tiles_pq.size() * sizeof(slorr::Tile));
+    put(p.off_tiles_prep, p.tiles_prep.data(), p.tiles_prep.size() * sizeof(slorr::Tile));
+    put(p.off_chunks, p.chunks.data(), p.chunks.size() * sizeof(slorr::Chunk));
+    hip_check(hipMemcpy(dev_ptr, host.data(), host.size(), hipMemcpyHostToDevice), "hipMemcpy tables");
+    for (int k = 0; k < 2; ++k) {
+      hip_check(hipHostMalloc(&p.staging[k], p.dyn_bytes(), hipHostMallocDefault), "hipHostMalloc");
+      hipEvent_t ev;
+      hip_check(hipEventCreateWithFlags(&ev, hipEventDisableTiming), "hipEventCreate");
+      p.staging_event[k] = ev;
+    }
+    p.device = dev;
+    p.ws = dev_ptr;
+    p.dyn_valid = false;
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const *weights,
+                                 const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                                 float *out_vals, float *const *out_grads, float grad_scale,
+                                 void *stream) {
+  return guarded([&]() -> slorr_status_t {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    slorr::Plan &p = prepare_call(plan, n, weights, shapes, kind, iters, out_vals, out_grads,
+                                  grad_scale, s);
+    if (p.flags & SLORR_NO_GRAPH) {
+      slorr::enqueue(p, s);
+      return SLORR_OK;
+    }
+    if (!p.graph_exec) {
+      hipStream_t cs;
+      hip_check(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking), "hipStreamCreate");
+      p.capture_stream = cs;
+      hip_check(hipStreamBeginCapture(cs, hipStreamCaptureModeRelaxed), "hipStreamBeginCapture");
+      try {
+        slorr::enqueue(p, cs);
+      } catch (...) {
+        hipGraph_t g = nullptr;
+        (void)hipStreamEndCapture(cs, &g);
+        if (g) (void)hipGraphDestroy(g);
+        throw;
+      }
+      hipGraph_t g = nullptr;
+      hip_check(hipStreamEndCapture(cs, &g), "hipStreamEndCapture");
+      p.graph = g;
+      hipGraphExec_t ge = nullptr;
+      hip_check(hipGraphInstantiate(&ge, g, nullptr, nullptr, 0), "hipGraphInstantiate");
+      p.graph_exec = ge;
+    }
+    hip_check(hipGraphLaunch(static_cast<hipGraphExec_t>(p.graph_exec), s), "hipGraphLaunch");
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
+                                          const void *const *weights, const slorr_shape_t *shapes,
+                                          slorr_kind_t kind, int32_t iters, float *out_vals,
+                                          float *const *out_grads, float grad_scale, void *stream,
+                                          float *launch_ms, int32_t *launch_op) {
+  return guarded([&]() -> slorr_status_t {
+    if (!launch_ms) throw std::invalid_argument("launch_ms is NULL");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    slorr::Plan &p = prepare_call(plan, n, weights, shapes, kind, iters, out_vals, out_grads,
+                                  grad_scale, s);
+    const size_t nl = p.launches.size();
+    std::vector<hipEvent_t> ev(2 * nl, nullptr);
+    struct Guard {
+      std::vector<hipEvent_t> &e;
+      ~Guard() {
+        for (auto x : e)
+          if (x) (void)hipEventDestroy(x);
+      }
+    } guard{ev};
+    for (auto &e : ev) hip_check(hipEventCreate(&e), "hipEventCreate");
+    slorr::enqueue(p, s, ev.data());
+    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+    for (size_t i = 0; i < nl; ++i) {
+      float ms = 0.0f;
+      hip_check(hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]), "hipEventElapsedTime");
+      launch_ms[i] = ms;
+      if (launch_op) launch_op[i] = int32_t(p.launches[i].op);
+    }
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_plan_destroy(slorr_plan_t plan) {
+  return guarded([&]() -> slorr_status_t {
+    if (!plan) return SLORR_OK;
+    release_runtime(plan->p);
+    delete plan;
+    return SLORR_OK;
+  });
+}
+
+const char *slorr_status_string(slorr_status_t s) {
+  switch (s) {
+    case SLORR_OK: return "SLORR_OK";
+    case SLORR_ERR_INVALID_ARGUMENT: return "SLORR_ERR_INVALID_ARGUMENT";
+    case SLORR_ERR_UNSUPPORTED: return "SLORR_ERR_UNSUPPORTED";
+    case SLORR_ERR_PLAN_MISMATCH: return "SLORR_ERR_PLAN_MISMATCH";
+    case SLORR_ERR_WORKSPACE: return "SLORR_ERR_WORKSPACE";
+    case SLORR_ERR_HIP: return "SLORR_ERR_HIP";
+    case SLORR_ERR_INTERNAL: return "SLORR_ERR_INTERNAL";
+  }
+  return "SLORR_UNKNOWN_STATUS";
+}
+
+const char *slorr_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,63 @@
+// Device-visible plan tables of the SLORR library (shared by host and kernels).
+//
+// Every matrix W_i (rows x cols, row-major) is iterated in its canonical "wide"
+// orientation P x Q, P = min(rows, cols), Q = max(rows, cols); the canonical
+// operand is W when rows <= cols and W^T otherwise (the short-side Gram product
+// behind the 4 P^2 Q + 2 P^3 cost of Sec. 3). Canonical buffers are zero-padded
+// to Pp x Qp (multiples of kTile) so that GEMM tiles never need bounds checks:
+// zero rows/columns stay zero under X <- a X + (b XX^T + c (XX^T)^2) X.
+#pragma once
+#include <stdint.h>
+
+namespace slorr {
+
+constexpr int kTile = 128;       // GEMM block tile (rows = cols) and padding granularity
+constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
+constexpr int kChunk = 8192;     // elements per block in the norm and gradient kernels
+constexpr int kThreads = 256;    // threads per block of every kernel
+
+// Power-of-two operand scales of the fp16 iterate (bf16 weights). With the
+// input normalised by ||W||_F every singular value of X stays <= u_t <= 2, so
+// |X_ij| <= 2, |A_ij| <= 4 and |B_ij| <= max |b t + c t^2| over t in [0, 4]
+// (< 9 for the default schedule); the scales keep these far below the fp16
+// maximum (65504) while moving the typical entries (~1/sqrt(PQ)) well into
+// the normal range.
+constexpr float kScaleX16 = 4096.0f;
+constexpr float kScaleA16 = 4096.0f;
+constexpr float kScaleB16 = 1024.0f;
+
+struct MatDesc {
+  int32_t rows, cols;          // original shape
+  int32_t P, Q, Pp, Qp;        // canonical and padded canonical shape
+  int32_t tall;                // 1 if the canonical operand is W^T
+  int32_t empty;               // rows == 0 or cols == 0
+  int32_t chunk_begin, chunk_end;   // slots in the norm-partials array
+  int32_t trace_begin, trace_end;   // slots in the trace-partials array
+  uint64_t x0, x1, a, b, pbuf;      // byte offsets in the workspace
+};
+
+struct DynDesc {               // per call: caller pointers
+  const void *w;
+  float *g;
+};
+
+struct CallParams {            // per call
+  float *out_vals;
+  float grad_scale;
+  int32_t pad;
+};
+
+struct Tile {                  // one GEMM output tile / one prep tile
+  int32_t mat, tm, tn, slot;
+};
+
+struct Chunk {                 // a contiguous run of a matrix's elements
+  int32_t mat, begin, len, pad;
+};
+
+struct Scalars {               // per matrix, written by the kernels
+  double sumsq, f, feps, nhat, value, c1, c2;
+  float inv_feps, pad;
+};
+
+}  // namespace slorr

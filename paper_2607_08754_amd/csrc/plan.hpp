@@ -1,0 +1,84 @@
+// Host-side plan: canonicalisation, shape grouping, tile/chunk lists and the
+// workspace layout. Integer metadata only; building a plan touches no device.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "layout.hpp"
+#include "slorr.h"
+
+namespace slorr {
+
+void greedy_schedule(double ell, int degree, int iters, double *out);
+
+// One kernel launch of the fixed schedule.
+enum class Op : int {
+  SumSq = SLORR_OP_SUMSQ,        // partial sums of squares per chunk
+  NormFin = SLORR_OP_NORM,       // f, f + eps per matrix
+  Prep = SLORR_OP_PREP,          // X_0 = W / (f + eps), canonical, padded
+  Gram = SLORR_OP_GRAM,          // A = X X^T
+  Poly = SLORR_OP_POLY,          // B = b A + c A A
+  Update = SLORR_OP_UPDATE,      // X' = a X + B X        (or a X + b A X when c = 0)
+  Last = SLORR_OP_LAST,          // final update: P, trace partials
+  Finalize = SLORR_OP_FINALIZE,  // values, set sum, gradient coefficients
+  Grad = SLORR_OP_GRAD           // grad = c1 P - c2 W   (original orientation)
+};
+
+struct Launch {
+  Op op;
+  int32_t grid;        // blocks
+  int32_t list;        // which tile list (0: gram/poly, 1: update, 2: prep)
+  int32_t which_x;     // current X buffer (0: x0, 1: x1)
+  int32_t use_a;       // update operand is A (cubic step) instead of B
+  float alpha, beta;   // epilogue coefficients
+};
+
+struct Plan {
+  // arguments
+  int32_t n = 0;
+  slorr_dtype_t dtype = SLORR_F32;
+  slorr_kind_t kind = SLORR_HOYER;
+  int32_t iters = 6, degree = 5;
+  double ell = 1e-3;
+  float eps = 0.0f;
+  uint32_t flags = 0;
+  std::vector<slorr_shape_t> shapes;
+  std::vector<double> coeffs;          // iters x 3
+  // derived
+  int32_t groups = 0;
+  std::vector<MatDesc> mats;
+  std::vector<Tile> tiles_pp;          // P x P outputs (gram, poly)
+  std::vector<Tile> tiles_pq;          // P x Q outputs (update, last)
+  std::vector<Tile> tiles_prep;        // prep tiles over Pp x Qp
+  std::vector<Chunk> chunks;           // original-layout element runs
+  std::vector<Launch> launches;
+  double paper_flops = 0, mfma_flops = 0, weight_bytes = 0;
+  // workspace layout (byte offsets)
+  size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles_pp = 0, off_tiles_pq = 0,
+         off_tiles_prep = 0, off_chunks = 0, off_scal = 0, off_sumsq = 0, off_trace = 0,
+         off_static_end = 0, ws_bytes = 0;
+  // runtime state (owned by the API layer)
+  void *ws = nullptr;
+  int device = -1;
+  void *graph = nullptr;       // hipGraph_t
+  void *graph_exec = nullptr;  // hipGraphExec_t
+  void *capture_stream = nullptr;
+  void *staging[2] = {nullptr, nullptr};  // pinned host buffers for the per-call tables
+  void *staging_event[2] = {nullptr, nullptr};
+  int staging_next = 0;
+  bool dyn_valid = false;
+  std::vector<DynDesc> dyn_cache;
+  CallParams call_cache{};
+
+  size_t elem_bytes() const { return dtype == SLORR_BF16 ? 2 : 4; }     // weights
+  size_t iter_bytes() const { return dtype == SLORR_BF16 ? 2 : 4; }     // X, A, B
+  size_t dyn_bytes() const;                                            // dyn table + call params
+};
+
+// Throws std::invalid_argument (bad input) or std::domain_error (unsupported).
+void build_plan(Plan &p);
+
+}  // namespace slorr

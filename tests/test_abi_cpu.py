@@ -1,0 +1,234 @@
+"""Host-side tests of the C ABI (no GPU needed): the library loads and exports
+every function include/slorr.h declares, the library's schedule generator
+agrees with the oracle's independent one, plans report the right facts, and
+every argument error is reported before anything touches a device.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle.pe_schedule import pe_schedule
+from workloads import CONFIGS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2607_08754_amd._lib as lib_mod
+    return lib_mod
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "slorr.h")).read()
+    return sorted(set(re.findall(r"SLORR_API\s+[\w\s\*]*?\b(slorr_\w+)\s*\(", text)))
+
+
+def test_exports_match_header(L):
+    declared = _declared_functions()
+    assert len(declared) >= 10
+    lib = L.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(L.EXPORTED) == declared
+    out = os.popen(f"nm -D --defined-only {L.LIB_PATH}").read()
+    exported = sorted(set(re.findall(r"\bT (slorr_\w+)", out)))
+    assert exported == declared                      # nothing else is exported
+
+
+def test_schedule_matches_oracle(L):
+    """Two independent Remez implementations (C++ library, NumPy oracle)."""
+    from paper_2607_08754_amd import pe_coefficients
+    for ell in (1e-3, 0.05, 0.3):
+        for d in (3, 5):
+            lib_tab = pe_coefficients(8, ell, d)
+            ora_tab = pe_schedule(8, ell, d)
+            # rows solved on narrow intervals (half-width ~1e-3) are limited by
+            # the conditioning of the Remez system, not by the method
+            assert np.allclose(lib_tab, ora_tab, rtol=1e-10, atol=1e-10), (ell, d)
+    # the paper's setting, T = 6: wide intervals, agreement to rounding
+    assert np.allclose(pe_coefficients(6), pe_schedule(6), rtol=1e-13, atol=0)
+
+
+def _plan(L, shapes, dtype=0, kind=0, opts=None):
+    lib = L.lib()
+    h = ctypes.c_void_p()
+    ws = ctypes.c_size_t()
+    arr = (L.Shape * max(1, len(shapes)))(*[L.Shape(r, c) for r, c in shapes])
+    st = lib.slorr_plan_create(ctypes.byref(h), len(shapes), arr, dtype, kind,
+                               ctypes.byref(opts) if opts is not None else None, ctypes.byref(ws))
+    return st, h, ws.value, arr
+
+
+@pytest.mark.parametrize("name", list(CONFIGS))
+def test_plan_facts(L, name):
+    cfg = CONFIGS[name]
+    lib = L.lib()
+    opts = L.Options()
+    lib.slorr_default_options(ctypes.byref(opts))
+    opts.iters = cfg.iters
+    st, h, ws, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER, opts)
+    assert st == L.OK, lib.slorr_last_error()
+    info = L.PlanInfo()
+    assert lib.slorr_plan_get_info(h, ctypes.byref(info)) == L.OK
+    assert info.n == cfg.n and info.iters == cfg.iters
+    assert info.paper_flops == pytest.approx(cfg.flops(), rel=1e-12)
+    assert info.mfma_flops >= info.paper_flops
+    assert info.groups == len({(min(s), max(s)) for s in cfg.shapes})
+    # sumsq, norm, prep, 3 GEMMs per step, finalize, grad
+    assert info.launches == 3 + 3 * cfg.iters + 2
+    assert info.workspace_bytes == ws > 0
+    esz = 2 if cfg.dtype == "bf16" else 4
+    assert info.weight_bytes == sum(r * c * esz for r, c in cfg.shapes)
+    assert lib.slorr_plan_destroy(h) == L.OK
+
+
+def test_plan_padding_waste_is_bounded(L):
+    """The headline sets are tile-aligned: no padded MFMA work at all."""
+    for name in ("vit_b16", "vit_l16", "llm560"):
+        cfg = CONFIGS[name]
+        st, h, _, _ = _plan(L, cfg.shapes, L.BF16, L.HOYER)
+        info = L.PlanInfo()
+        L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+        assert info.mfma_flops == pytest.approx(info.paper_flops * (cfg.iters / 6), rel=1e-12) or \
+            info.mfma_flops == pytest.approx(info.paper_flops, rel=1e-12)
+        L.lib().slorr_plan_destroy(h)
+
+
+def test_empty_plans(L):
+    st, h, ws, _ = _plan(L, [])
+    assert st == L.OK and ws > 0
+    L.lib().slorr_plan_destroy(h)
+    st, h, ws, _ = _plan(L, [(0, 7), (5, 0)])
+    assert st == L.OK
+    info = L.PlanInfo()
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.launches == 2 and info.gemm_tiles == 0       # norm + finalize
+    L.lib().slorr_plan_destroy(h)
+
+
+def test_plan_create_errors(L):
+    lib = L.lib()
+    h = ctypes.c_void_p(1234)
+    ws = ctypes.c_size_t()
+    one = (L.Shape * 1)(L.Shape(4, 8))
+    # null out-pointers / shapes, negative n
+    assert lib.slorr_plan_create(None, 1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan_create(ctypes.byref(h), 1, one, 0, 0, None, None) == L.ERR_INVALID_ARGUMENT
+    assert h.value is None                                    # set to NULL on error
+    assert lib.slorr_plan_create(ctypes.byref(h), 1, None, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan_create(ctypes.byref(h), -1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert b"n must be" in lib.slorr_last_error()
+    # bad shapes
+    for r, c, want in [(-1, 4, L.ERR_INVALID_ARGUMENT), (16385, 16385, L.ERR_UNSUPPORTED),
+                       (4, (1 << 20) + 1, L.ERR_UNSUPPORTED), (16384, 1 << 20, L.ERR_UNSUPPORTED)]:
+        st, _, _, _ = _plan(L, [(r, c)])
+        assert st == want, (r, c, st)
+    # dtype / kind
+    assert _plan(L, [(4, 8)], dtype=7)[0] == L.ERR_UNSUPPORTED
+    assert _plan(L, [(4, 8)], kind=9)[0] == L.ERR_UNSUPPORTED
+    # options
+    def with_opts(**kw):
+        o = L.Options()
+        lib.slorr_default_options(ctypes.byref(o))
+        for k, v in kw.items():
+            setattr(o, k, v)
+        return _plan(L, [(4, 8)], opts=o)[0]
+    assert with_opts(iters=-2) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(iters=5000) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(degree=7) == L.ERR_UNSUPPORTED
+    assert with_opts(ell=1.5) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(ell=-0.1) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(eps=-1.0) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(eps=float("inf")) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(flags=0x100) == L.ERR_INVALID_ARGUMENT
+    bad = (ctypes.c_double * 18)(*([1.0] * 17 + [float("nan")]))
+    assert with_opts(coeffs=ctypes.cast(bad, ctypes.POINTER(ctypes.c_double))) == L.ERR_INVALID_ARGUMENT
+    assert with_opts() == L.OK
+
+
+def test_pe_coefficients_errors(L):
+    lib = L.lib()
+    out = (ctypes.c_double * 30)()
+    assert lib.slorr_pe_coefficients(1e-3, 5, 6, None) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_pe_coefficients(1e-3, 4, 6, out) == L.ERR_UNSUPPORTED
+    assert lib.slorr_pe_coefficients(0.0, 5, 6, out) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_pe_coefficients(1e-3, 5, 0, out) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_pe_coefficients(1e-3, 5, 10, out) == L.OK
+
+
+def test_call_errors_before_any_device_use(L):
+    """Argument checks of slorr_reg_fwd_bwd run before the workspace check and
+    before any HIP call, so they are testable on a machine without a GPU."""
+    lib = L.lib()
+    st, h, ws, shapes = _plan(L, [(4, 8), (8, 4)])
+    assert st == L.OK
+    vals = ctypes.c_void_p(0x10000)
+    w = (ctypes.c_void_p * 2)(0x20000, 0x30000)
+    g = (ctypes.c_void_p * 2)(0x40000, 0x50000)
+    call = lib.slorr_reg_fwd_bwd
+    assert call(None, 2, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 3, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert call(h, 2, w, shapes, 1, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert call(h, 2, w, shapes, 0, 5, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    other = (L.Shape * 2)(L.Shape(4, 8), L.Shape(4, 8))
+    assert call(h, 2, w, other, 0, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert call(h, 2, w, shapes, 0, 6, None, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 2, w, shapes, 0, 6, ctypes.c_void_p(0x10001), g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 2, None, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 2, w, shapes, 0, 6, vals, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    misaligned = (ctypes.c_void_p * 2)(0x20008, 0x30000)
+    assert call(h, 2, misaligned, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    nullw = (ctypes.c_void_p * 2)(0x20000, None)
+    assert call(h, 2, nullw, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    # gradient 0 (4x8 fp32 = 128 B at 0x40000) overlaps gradient 1
+    overlap = (ctypes.c_void_p * 2)(0x40000, 0x40040)
+    assert call(h, 2, w, shapes, 0, 6, vals, overlap, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    alias = (ctypes.c_void_p * 2)(0x20000, 0x50000)              # grad 0 == weight 0
+    assert call(h, 2, w, shapes, 0, 6, vals, alias, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    # weights may overlap each other (read only); then: no workspace attached
+    shared_w = (ctypes.c_void_p * 2)(0x20000, 0x20000)
+    assert call(h, 2, shared_w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_WORKSPACE
+    assert call(h, 2, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_WORKSPACE
+    assert b"workspace" in lib.slorr_last_error()
+    ms = (ctypes.c_float * 32)()
+    assert lib.slorr_reg_fwd_bwd_profiled(h, 2, w, shapes, 0, 6, vals, g, 1.0, None, None, None) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_reg_fwd_bwd_profiled(h, 2, w, shapes, 0, 6, vals, g, 1.0, None, ms, None) == L.ERR_WORKSPACE
+    # workspace checks that precede any device call
+    assert lib.slorr_plan_set_workspace(h, None, ws) == L.ERR_WORKSPACE
+    assert lib.slorr_plan_set_workspace(h, ctypes.c_void_p(0x1000 + 16), ws) == L.ERR_WORKSPACE
+    assert lib.slorr_plan_set_workspace(h, ctypes.c_void_p(0x1000), ws - 1) == L.ERR_WORKSPACE
+    assert lib.slorr_plan_destroy(h) == L.OK
+    assert lib.slorr_plan_destroy(None) == L.OK
+
+
+def test_values_only_accepts_null_grads(L):
+    lib = L.lib()
+    o = L.Options()
+    lib.slorr_default_options(ctypes.byref(o))
+    o.flags = L.VALUES_ONLY
+    st, h, _, shapes = _plan(L, [(4, 8)], opts=o)
+    assert st == L.OK
+    w = (ctypes.c_void_p * 1)(0x20000)
+    assert lib.slorr_reg_fwd_bwd(h, 1, w, shapes, 0, 6, ctypes.c_void_p(0x10000), None, 1.0, None) == L.ERR_WORKSPACE
+    lib.slorr_plan_destroy(h)
+
+
+def test_status_strings(L):
+    lib = L.lib()
+    for code in range(7):
+        assert lib.slorr_status_string(code).startswith(b"SLORR_")
+    assert lib.slorr_status_string(99) == b"SLORR_UNKNOWN_STATUS"
+
+
+def test_binding_validates_in_python(L):
+    """The Python wrapper rejects mismatched tensors before calling the ABI."""
+    from paper_2607_08754_amd import Plan
+    p = Plan([(4, 8)], dtype="f32", create_workspace=False)
+    with pytest.raises(RuntimeError):
+        p([np.zeros((4, 8))], None)
+    assert p.info()["n"] == 1
+    p.close()

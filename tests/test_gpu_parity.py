@@ -1,0 +1,224 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU fp64 oracle on
+the same seeded inputs, element by element (per-matrix values and full
+gradients), for every configured weight set and the edge cases.
+"""
+import numpy as np
+import pytest
+
+from parity_util import TOL, compare, run_gpu, run_oracle, to_device
+from workloads import CONFIGS, gaussian, make_set
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    import paper_2607_08754_amd._lib as L
+    L.lib()          # fail loudly if the library is missing
+
+
+@pytest.mark.parametrize("kind", ["hoyer", "nuclear"])
+def test_tiny(kind):
+    cfg = CONFIGS["tiny"]
+    arrs = make_set("tiny", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, kind, cfg.iters)
+    refs = run_oracle(arrs, cfg.dtype, kind, cfg.iters)
+    compare(vals, grads, refs, kind, cfg.dtype, label="tiny")
+
+
+@pytest.mark.parametrize("kind", ["hoyer", "nuclear"])
+def test_resnet18(kind):
+    cfg = CONFIGS["resnet18"]
+    arrs = make_set("resnet18", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, kind, cfg.iters)
+    refs = run_oracle(arrs, cfg.dtype, kind, cfg.iters)
+    compare(vals, grads, refs, kind, cfg.dtype, label="resnet18")
+
+
+@pytest.mark.parametrize("kind", ["hoyer", "nuclear"])
+def test_vit_b16(kind):
+    """The benchmarked set, full size, graph replay as timed."""
+    cfg = CONFIGS["vit_b16"]
+    arrs = make_set("vit_b16", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, kind, cfg.iters)
+    refs = run_oracle(arrs, cfg.dtype, kind, cfg.iters)
+    compare(vals, grads, refs, kind, cfg.dtype, label="vit_b16")
+
+
+@pytest.mark.slow
+def test_vit_l16_sampled():
+    """Full set on the GPU; one block (4 matrices) and the last block checked."""
+    cfg = CONFIGS["vit_l16"]
+    arrs = make_set("vit_l16", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, "hoyer", cfg.iters)
+    idx = [0, 1, 2, 3, cfg.n - 1]
+    refs = run_oracle([arrs[i] for i in idx], cfg.dtype, "hoyer", cfg.iters)
+    compare(np.array([vals[i] for i in idx] + [0.0]), [grads[i] for i in idx], refs, "hoyer",
+            cfg.dtype, label="vit_l16 sample", check_total=False)
+
+
+@pytest.mark.slow
+def test_llm560_sampled():
+    """Full 168-matrix set on the GPU; the 7 matrices of layer 0 and the last
+    down projection checked against the oracle."""
+    cfg = CONFIGS["llm560"]
+    arrs = make_set("llm560", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, "hoyer", cfg.iters)
+    idx = list(range(7)) + [cfg.n - 1]
+    refs = run_oracle([arrs[i] for i in idx], cfg.dtype, "hoyer", cfg.iters)
+    compare(np.array([vals[i] for i in idx] + [0.0]), [grads[i] for i in idx], refs, "hoyer",
+            cfg.dtype, label="llm560 sample", check_total=False)
+
+
+RAGGED = [(7, 13), (13, 7), (130, 257), (257, 130), (1, 300), (300, 1), (128, 128), (129, 129),
+          (64, 64), (200, 1000), (1000, 200), (1, 1), (255, 384)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["hoyer", "nuclear"])
+def test_ragged_shapes(dtype, kind):
+    arrs = [gaussian(s, seed=100, std=0.05, dtype=dtype, index=i) for i, s in enumerate(RAGGED)]
+    vals, grads, _ = run_gpu(arrs, dtype, kind, 6, eps=1e-3, g=0.37)
+    refs = run_oracle(arrs, dtype, kind, 6, eps=1e-3, g=0.37)
+    compare(vals, grads, refs, kind, dtype, g=0.37, label=f"ragged {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_empty_and_zero_matrices(dtype):
+    import torch
+    from paper_2607_08754_amd import Plan
+    shapes = [(0, 5), (6, 0), (33, 70), (40, 9)]
+    arrs = [np.zeros((0, 5), np.float32), np.zeros((6, 0), np.float32),
+            gaussian((33, 70), seed=3, std=1.0, dtype="f32"), np.zeros((40, 9), np.float32)]
+    if dtype == "bf16":
+        from workloads import f32_to_bf16_bits
+        arrs = [f32_to_bf16_bits(a) for a in arrs]
+    for eps in (0.0, 1e-6):
+        vals, grads, _ = run_gpu(arrs, dtype, "hoyer", 6, eps=eps)
+        refs = run_oracle(arrs, dtype, "hoyer", 6, eps=eps)
+        assert vals[0] == 0.0 and vals[1] == 0.0 and vals[3] == 0.0
+        assert np.all(grads[3] == 0.0)
+        compare(vals, grads, refs, "hoyer", dtype, label=f"empty/zero eps={eps}")
+    # an all-empty set and n == 0
+    p = Plan([], dtype=dtype)
+    v = p([], [])
+    torch.cuda.synchronize()
+    assert v.cpu().numpy()[0] == 0.0
+
+
+def test_empty_set_values_only():
+    import torch
+    from paper_2607_08754_amd import Plan
+    p = Plan([(0, 3)], dtype="f32", values_only=True, aux=True)
+    empty = torch.zeros((0, 3), dtype=torch.float32, device="cuda:0")
+    v = p([empty]).cpu().numpy()
+    assert np.all(v == 0.0) and v.size == 4
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_flags_accumulate_values_only_aux(dtype):
+    import torch
+    from paper_2607_08754_amd import Plan
+    shapes = [(96, 200), (300, 140)]
+    arrs = [gaussian(s, seed=7, std=0.1, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+    refs = run_oracle(arrs, dtype, "hoyer", 6, g=2.5)
+    W = to_device(arrs, dtype, "cuda:0")
+    # accumulate: grad += g * dL/dW
+    p = Plan(shapes, dtype=dtype, accumulate=True, aux=True)
+    base = [torch.full(s, 0.75, dtype=torch.float32, device="cuda:0") for s in shapes]
+    v = p(W, base, grad_scale=2.5).cpu().numpy()
+    torch.cuda.synchronize()
+    for i, r in enumerate(refs):
+        got = base[i].cpu().numpy().astype(np.float64) - 0.75
+        assert np.linalg.norm(got - r.grad) <= TOL[dtype] * np.linalg.norm(r.grad) + 1e-6
+        assert abs(v[3 + i] - r.n_hat) <= TOL[dtype] * abs(r.n_hat)          # aux n_hat
+        assert abs(v[5 + i] - r.f) <= 1e-6 * r.f                            # aux ||W||_F
+    # values only
+    q = Plan(shapes, dtype=dtype, values_only=True)
+    vq = q(W).cpu().numpy()
+    for i, r in enumerate(refs):
+        assert abs(vq[i] - r.value) <= TOL[dtype] * abs(r.value)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_graph_equals_eager_and_determinism(dtype):
+    import torch
+    from paper_2607_08754_amd import Plan
+    shapes = [(256, 640), (640, 256), (130, 130)]
+    arrs = [gaussian(s, seed=11, std=0.02, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+    W = to_device(arrs, dtype, "cuda:0")
+    outs = []
+    for graph in (True, False):
+        p = Plan(shapes, dtype=dtype, graph=graph)
+        for rep in range(3):
+            G = [torch.empty(s, dtype=torch.float32, device="cuda:0") for s in shapes]
+            v = p(W, G)
+            torch.cuda.synchronize()
+            outs.append((v.cpu().numpy(), [g.cpu().numpy() for g in G]))
+    for v, gs in outs[1:]:
+        assert np.array_equal(v, outs[0][0])
+        for a, b in zip(gs, outs[0][1]):
+            assert np.array_equal(a, b)
+
+
+def test_pointer_change_between_calls():
+    """New weight / gradient tensors between replays of one plan."""
+    import torch
+    from paper_2607_08754_amd import Plan
+    shapes = [(64, 192), (192, 64)]
+    p = Plan(shapes, dtype="f32")
+    for seed in (1, 2, 3):
+        arrs = [gaussian(s, seed=seed, std=0.3, dtype="f32", index=i) for i, s in enumerate(shapes)]
+        vals, grads, _ = run_gpu(arrs, "f32", "hoyer", 6, plan=p)
+        refs = run_oracle(arrs, "f32", "hoyer", 6)
+        compare(vals, grads, refs, "hoyer", "f32", label=f"pointer change {seed}")
+
+
+def test_grad_scale_changes_between_replays():
+    import torch
+    from paper_2607_08754_amd import Plan
+    shapes = [(50, 120)]
+    arrs = [gaussian(shapes[0], seed=5, std=1.0, dtype="f32")]
+    W = to_device(arrs, "f32", "cuda:0")
+    G = [torch.empty(shapes[0], dtype=torch.float32, device="cuda:0")]
+    p = Plan(shapes, dtype="f32")
+    p(W, G, grad_scale=1.0)
+    g1 = G[0].cpu().numpy().copy()
+    p(W, G, grad_scale=-3.0)
+    g3 = G[0].cpu().numpy()
+    assert np.allclose(g3, -3.0 * g1, rtol=1e-6, atol=1e-12)
+
+
+def test_cubic_and_explicit_coefficients():
+    """Degree 3 schedule (c_t = 0 skips the A A product) and an explicit
+    table (classical Newton-Schulz quintic, repeated)."""
+    from oracle.pe_schedule import pe_schedule
+    shapes = [(80, 150), (150, 80)]
+    arrs = [gaussian(s, seed=21, std=1.0, dtype="f32", index=i) for i, s in enumerate(shapes)]
+    vals, grads, _ = run_gpu(arrs, "f32", "hoyer", 8, degree=3)
+    refs = run_oracle(arrs, "f32", "hoyer", 8, table=pe_schedule(8, d=3))
+    compare(vals, grads, refs, "hoyer", "f32", label="cubic")
+    ns5 = np.repeat(np.array([[1.875, -1.25, 0.375]]), 10, axis=0)
+    vals, grads, _ = run_gpu(arrs, "f32", "nuclear", 10, coeffs=ns5)
+    refs = run_oracle(arrs, "f32", "nuclear", 10, table=ns5)
+    compare(vals, grads, refs, "nuclear", "f32", label="ns5 table")
+
+
+def test_plan_mismatch_and_overlap_errors():
+    import torch
+    from paper_2607_08754_amd import Plan, SlorrError
+    import paper_2607_08754_amd._lib as L
+    shapes = [(32, 48), (48, 32)]
+    p = Plan(shapes, dtype="f32")
+    W = [torch.randn(s, device="cuda:0") for s in shapes]
+    big = torch.empty(4096, device="cuda:0")
+    G_alias = [big[:32 * 48].view(32, 48), big[32 * 48 - 4:32 * 48 - 4 + 48 * 32].view(48, 32)]
+    with pytest.raises(SlorrError) as e:
+        p(W, G_alias)
+    assert e.value.status == L.ERR_INVALID_ARGUMENT
+    with pytest.raises(SlorrError) as e:
+        p(W, [W[0], torch.empty(48, 32, device="cuda:0")])      # grads alias weights (same dtype f32)
+    assert e.value.status == L.ERR_INVALID_ARGUMENT
