@@ -189,7 +189,9 @@ def test_grad_scale_changes_between_replays():
     g1 = G[0].cpu().numpy().copy()
     p(W, G, grad_scale=-3.0)
     g3 = G[0].cpu().numpy()
-    assert np.allclose(g3, -3.0 * g1, rtol=1e-6, atol=1e-12)
+    # c1 = g s1 and c2 = g s2 are rounded to fp32 per call, and the Hoyer
+    # gradient is a difference of two terms: compare on the gradient's scale
+    assert np.allclose(g3, -3.0 * g1, rtol=1e-5, atol=1e-6 * np.abs(g3).max())
 
 
 def test_cubic_and_explicit_coefficients():
