@@ -268,9 +268,7 @@ slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t
       if (n) std::memcpy(host.data() + off, src, n);
     };
     put(p.off_mats, p.mats.data(), p.mats.size() * sizeof(slorr::MatDesc));
-    put(p.off_tiles_pp, p.tiles_pp.data(), p.tiles_pp.size() * sizeof(slorr::Tile));
-    put(p.off_tiles_pq, p.tiles_pq.data(), p.tiles_pq.size() * sizeof(slorr::Tile));
-    put(p.off_tiles_prep, p.tiles_prep.data(), p.tiles_prep.size() * sizeof(slorr::Tile));
+    put(p.off_tiles, p.tiles.data(), p.tiles.size() * sizeof(slorr::Tile));
     put(p.off_chunks, p.chunks.data(), p.chunks.size() * sizeof(slorr::Chunk));
     hip_check(hipMemcpy(dev_ptr, host.data(), host.size(), hipMemcpyHostToDevice), "hipMemcpy tables");
     for (int k = 0; k < 2; ++k) {

@@ -1,0 +1,389 @@
+// MFMA GEMM core of the Polar Express step (device code, included by
+// kernels.hip). One launch covers every matrix of the set: each block takes
+// one output tile from the launch's tile list.
+//
+//   Gram    A  = X X^T                 NT: both operands are rows of X (k = Q)
+//   Poly    B  = b A + c A A^T         NT on the symmetric A (A A^T = A A)
+//   Update  X' = a X + B X             B symmetric (rows of B = columns of B);
+//                                      X is read as [k][n] and transposed into
+//                                      the K-major LDS layout on the way in
+//   Last    X_T = a X + B X, stored like an update, with the per-tile partial
+//           sums of W * P (P = X_T in fp32; the trace of W^T P) read against W
+//           in its own orientation
+//
+// Gram and Poly outputs are symmetric: only tiles with tm <= tn are computed
+// and off-diagonal tiles are also stored transposed (mirror).
+//
+// LDS layout: each operand row of a k-slab is 128 bytes (64 fp16 or 32 fp32
+// values of consecutive k) split into eight 16-byte chunks stored at chunk
+// index (c ^ (row & 7)). A wave's 16-byte fragment reads touch 8 consecutive
+// rows per 8-lane phase, which then land in 8 distinct bank groups; the
+// stores of the NK loader (8 lanes per row) and of the transposing KN loader
+// (16 lanes per row, 8-byte pieces) are conflict-free too.
+//
+// Pipeline: two LDS stages, one barrier per k-slab; the global loads of slab
+// k+1 are in flight while the MFMAs of slab k run.
+// Included inside namespace slorr, after the helpers of kernels.hip.
+#pragma once
+
+// MFMA per operand type. A lane feeds 16 bytes of one row of each operand
+// (8 fp16 or 4 fp32 consecutive k); lanes 0-31 and 32-63 take the two halves
+// of a 16 (fp16) / 8 (fp32) wide k step. Both operands use the same lane -> k
+// map, so the instruction's internal k order does not matter for the sum.
+template <typename T> struct Mfma;
+template <> struct Mfma<_Float16> {
+  typedef half8 frag;
+  static constexpr int V = 8;
+  __device__ static __forceinline__ void mma(floatx16 &c, const frag &a, const frag &b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<float> {
+  typedef float4v frag;
+  static constexpr int V = 4;
+  __device__ static __forceinline__ void mma(floatx16 &c, const frag &a, const frag &b) {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2], b[2], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[3], b[3], c, 0, 0, 0);
+  }
+};
+
+enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2, kLast = 3 };
+
+struct GemmArgs {
+  const Tile *tiles;
+  const MatDesc *mats;
+  const DynDesc *dyn;
+  char *ws;
+  double *tpart;
+  int which_x;    // current X buffer
+  int use_a;      // update operand is A (cubic step)
+  int write_x;    // Last: store X_T (the gradient kernel reads it)
+  float alpha, beta, inv_sx;
+};
+
+template <int BM, int BN, int WGM, int WGN>
+struct GemmShape {
+  static constexpr int kWaves = WGM * WGN;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
+  static constexpr int FM = WTM / 32, FN = WTN / 32;     // 32x32 MFMA tiles per wave
+  static constexpr int kStage = (BM + BN) * 128;         // bytes per LDS stage
+  static constexpr int kEpiPitch = WTN + 4;              // floats per staged row
+  static constexpr int kEpiWave = 32 * kEpiPitch * 4;    // staged bytes per wave
+  static constexpr int kSmem = (2 * kStage > kWaves * kEpiWave) ? 2 * kStage : kWaves * kEpiWave;
+};
+
+// Byte offset of 16-byte chunk `chunk` of LDS row `row`. The XOR key
+// (row & 7) ^ ((row >> 3) & 1) permutes the chunks so that (a) any 8
+// consecutive rows (one 8-lane phase of a 16-byte read with 32 banks) use 8
+// distinct chunk positions, and (b) any 16 consecutive rows (a 16-lane phase
+// with 64 banks, where rows of equal parity share a 128-byte bank half) use 8
+// distinct positions per parity.
+__device__ __forceinline__ int swz_key(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+__device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ swz_key(row)) << 4); }
+
+// sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
+template <typename Tw>
+__device__ __forceinline__ double dot_w(const Tw *w, const float (&v)[8], int n) {
+  float wv[8];
+  if (n == 8 && (reinterpret_cast<uintptr_t>(w) & 15) == 0) {
+    if constexpr (sizeof(Tw) == 2) {
+      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+      const u16x8 h = *reinterpret_cast<const u16x8 *>(w);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) wv[j] = to_f(Tw(h[j]));
+    } else {
+      const float4v a = reinterpret_cast<const float4v *>(w)[0];
+      const float4v b = reinterpret_cast<const float4v *>(w)[1];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        wv[j] = a[j];
+        wv[4 + j] = b[j];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) wv[j] = j < n ? to_f(w[j]) : 0.0f;
+  }
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wv[j]);
+  return s;
+}
+
+// 8 consecutive values of type T from global memory (16-byte aligned).
+template <typename T>
+__device__ __forceinline__ void load8(const T *p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    const half8 h = *reinterpret_cast<const half8 *>(p);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = float(h[j]);
+  } else {
+    const float4v a = reinterpret_cast<const float4v *>(p)[0];
+    const float4v b = reinterpret_cast<const float4v *>(p)[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = a[j];
+      v[4 + j] = b[j];
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    half8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = _Float16(v[j]);
+    *reinterpret_cast<half8 *>(p) = h;
+  } else {
+    float4v a, b;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      a[j] = v[j];
+      b[j] = v[4 + j];
+    }
+    reinterpret_cast<float4v *>(p)[0] = a;
+    reinterpret_cast<float4v *>(p)[1] = b;
+  }
+}
+
+template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
+  using S = GemmShape<BM, BN, WGM, WGN>;
+  constexpr int NT = S::kThreads;
+  constexpr int V = Mfma<T>::V;
+  constexpr int BK = 8 * V;                      // k per slab (128-byte rows)
+  constexpr int FM = S::FM, FN = S::FN, WTM = S::WTM, WTN = S::WTN;
+  constexpr bool KN = (MODE == kUpdate || MODE == kLast);
+  constexpr int CA = BM * 8 / NT;                // 16-byte chunks per thread, A slab
+  constexpr int CB = BN * 8 / NT;                // same, B slab (NK)
+  constexpr int QB = (BK / 4) * (BN / V) / NT;   // 4 x V blocks per thread, B slab (KN)
+  static_assert(CA * NT == BM * 8 && CB * NT == BN * 8, "tile / thread mismatch");
+  static_assert(!KN || QB * NT == (BK / 4) * (BN / V), "KN loader mismatch");
+  static_assert(FM >= 1 && FN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+  typedef typename Mfma<T>::frag frag;
+  typedef T quad_t __attribute__((ext_vector_type(4)));
+  __shared__ __attribute__((aligned(16))) char smem[S::kSmem];
+
+  const Tile tile = args.tiles[blockIdx.x];
+  if (tile.mat < 0) return;      // padding of the XCD-ordered list (whole block)
+  const MatDesc d = args.mats[tile.mat];
+  const int m0 = tile.tm * BM, n0 = tile.tn * BN;
+  T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
+  T *Xn = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x0 : d.x1));
+  T *Am = reinterpret_cast<T *>(args.ws + d.a);
+  T *Bm = reinterpret_cast<T *>(args.ws + d.b);
+
+  const T *Ap;
+  const T *Bp;
+  int lda, ldb, K;
+  if (MODE == kGram) {
+    Ap = Xc; Bp = Xc; lda = ldb = d.Qp; K = d.Qp;
+  } else if (MODE == kPoly) {
+    Ap = Am; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
+  } else {
+    Ap = args.use_a ? Am : Bm; Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
+  }
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lk = lane >> 5;
+  const int wm = wave / WGN, wn = wave % WGN;
+
+  frag ra[CA];
+  frag rb[KN ? 4 * QB : CB];
+
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i) {
+      const int q = tid + i * NT, row = q >> 3, c = q & 7;
+      ra[i] = *reinterpret_cast<const frag *>(Ap + size_t(m0 + row) * lda + k0 + c * V);
+    }
+    if constexpr (!KN) {
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        const int q = tid + i * NT, row = q >> 3, c = q & 7;
+        rb[i] = *reinterpret_cast<const frag *>(Bp + size_t(n0 + row) * ldb + k0 + c * V);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          rb[4 * i + r] = *reinterpret_cast<const frag *>(Bp + size_t(k0 + 4 * kq + r) * ldb + n0 + nc * V);
+      }
+    }
+  };
+  auto sstore = [&](int buf) {
+    char *sA = smem + buf * S::kStage;
+    char *sB = sA + BM * 128;
+#pragma unroll
+    for (int i = 0; i < CA; ++i) {
+      const int q = tid + i * NT, row = q >> 3, c = q & 7;
+      *reinterpret_cast<frag *>(sA + swz(row, c)) = ra[i];
+    }
+    if constexpr (!KN) {
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        const int q = tid + i * NT, row = q >> 3, c = q & 7;
+        *reinterpret_cast<frag *>(sB + swz(row, c)) = rb[i];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
+        const int byte = 4 * kq * int(sizeof(T));          // offset of k = 4 kq in the row
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int n = nc * V + j;
+          quad_t v;
+          v[0] = rb[4 * i + 0][j];
+          v[1] = rb[4 * i + 1][j];
+          v[2] = rb[4 * i + 2][j];
+          v[3] = rb[4 * i + 3][j];
+          *reinterpret_cast<quad_t *>(sB + swz(n, byte >> 4) + (byte & 15)) = v;
+        }
+      }
+    }
+  };
+
+  floatx16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  auto compute = [&](int buf) {
+    const char *sA = smem + buf * S::kStage;
+    const char *sB = sA + BM * 128;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      frag fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        fa[i] = *reinterpret_cast<const frag *>(sA + swz(wm * WTM + i * 32 + lr, 2 * s + lk));
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        fb[j] = *reinterpret_cast<const frag *>(sB + swz(wn * WTN + j * 32 + lr, 2 * s + lk));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) Mfma<T>::mma(acc[i][j], fa[i], fb[j]);
+    }
+  };
+
+  const int nk = K / BK;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + 1 < nk) gload((kt + 1) * BK);
+    compute(kt & 1);
+    if (kt + 1 < nk) sstore((kt + 1) & 1);
+    __syncthreads();
+  }
+
+  // ------------------------------------------------------------ epilogue
+  // acc[i][j][r] holds row 8 (r / 4) + 4 lk + r % 4 and column lr of MFMA tile
+  // (i, j). Per 32-row block of the wave tile: stage in LDS (fp32), then
+  // finish row-wise with 16-byte accesses, then (mirror tiles, tall P) write
+  // the transpose column-wise.
+  constexpr int P = S::kEpiPitch;
+  constexpr int CG = WTN / 8;                     // 8-column groups per staged row
+  float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
+  const float alpha = args.alpha, beta = args.beta;
+  const bool mirror = (MODE == kGram || MODE == kPoly) && tile.tm != tile.tn;
+  const bool colwise = mirror || (MODE == kLast && d.tall);
+  double tsum = 0.0;
+  const Tw *W = (MODE == kLast) ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
+
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ep[(8 * (r >> 2) + 4 * lk + (r & 3)) * P + j * 32 + lr] = acc[i][j][r];
+    __syncthreads();
+    const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
+    for (int task = lane; task < 32 * CG; task += 64) {
+      const int row = task / CG, cg = task % CG;
+      float4v *e = reinterpret_cast<float4v *>(ep + row * P + cg * 8);
+      float v[8];
+      {
+        const float4v e0 = e[0], e1 = e[1];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[j] = e0[j];
+          v[4 + j] = e1[j];
+        }
+      }
+      const int grow = grow0 + row, gcol = gcol0 + cg * 8;
+      if (MODE == kGram) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] *= alpha;
+        store8(Am + size_t(grow) * d.Pp + gcol, v);
+      } else if (MODE == kPoly) {
+        float in[8];
+        load8(Am + size_t(grow) * d.Pp + gcol, in);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
+        store8(Bm + size_t(grow) * d.Pp + gcol, v);
+      } else {
+        float in[8];
+        load8(Xc + size_t(grow) * d.Qp + gcol, in);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
+        if (MODE == kUpdate || args.write_x) store8(Xn + size_t(grow) * d.Qp + gcol, v);
+        if (MODE == kLast) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
+          // wide W: canonical (m, n) = W[m][n], contiguous along the row
+          if (!d.tall && grow < d.P && gcol < d.Q)
+            tsum += dot_w(W + size_t(grow) * d.cols + gcol, v, min(8, d.Q - gcol));
+        }
+      }
+      if (colwise) {
+        float4v e0, e1;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          e0[j] = v[j];
+          e1[j] = v[4 + j];
+        }
+        e[0] = e0;
+        e[1] = e1;
+      }
+    }
+    __syncthreads();
+    if (colwise) {
+      // transpose: output row = this tile's column, 8 consecutive source rows
+      for (int task = lane; task < WTN * 4; task += 64) {
+        const int rg = task & 3, col = task >> 2;
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = ep[(rg * 8 + j) * P + col];
+        const int orow = gcol0 + col, ocol = grow0 + rg * 8;
+        if (MODE == kGram) {
+          store8(Am + size_t(orow) * d.Pp + ocol, v);
+        } else if (MODE == kPoly) {
+          store8(Bm + size_t(orow) * d.Pp + ocol, v);
+        } else if (MODE == kLast) {
+          // tall W: canonical (m, n) = W[n][m]; here n = orow, m = ocol + j,
+          // contiguous along W's row
+          if (orow < d.Q && ocol < d.P)
+            tsum += dot_w(W + size_t(orow) * d.cols + ocol, v, min(8, d.P - ocol));
+        }
+      }
+      __syncthreads();
+    }
+  }
+  if (MODE == kLast) {
+    const double r = block_sum<NT>(tsum, reinterpret_cast<double *>(smem));
+    if (tid == 0) args.tpart[tile.slot] = r;
+  }
+}

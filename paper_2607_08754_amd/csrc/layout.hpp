@@ -11,10 +11,12 @@
 
 namespace slorr {
 
-constexpr int kTile = 128;       // GEMM block tile (rows = cols) and padding granularity
+constexpr int kTile = 128;       // padding granularity = the small GEMM block tile
+constexpr int kBigTile = 256;    // the large GEMM block tile
 constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
 constexpr int kChunk = 8192;     // elements per block in the norm and gradient kernels
-constexpr int kThreads = 256;    // threads per block of every kernel
+constexpr int kThreads = 256;    // threads per block of the non-GEMM kernels
+constexpr int kXcds = 8;         // XCDs of an MI355X; workgroup b runs on XCD b % 8
 
 // Power-of-two operand scales of the fp16 iterate (bf16 weights). With the
 // input normalised by ||W||_F every singular value of X stays <= u_t <= 2, so
@@ -33,7 +35,7 @@ struct MatDesc {
   int32_t empty;               // rows == 0 or cols == 0
   int32_t chunk_begin, chunk_end;   // slots in the norm-partials array
   int32_t trace_begin, trace_end;   // slots in the trace-partials array
-  uint64_t x0, x1, a, b, pbuf;      // byte offsets in the workspace
+  uint64_t x0, x1, a, b;            // byte offsets in the workspace
 };
 
 struct DynDesc {               // per call: caller pointers
@@ -48,7 +50,7 @@ struct CallParams {            // per call
 };
 
 struct Tile {                  // one GEMM output tile / one prep tile
-  int32_t mat, tm, tn, slot;
+  int32_t mat, tm, tn, slot;   // mat < 0: padding entry, the block exits at once
 };
 
 struct Chunk {                 // a contiguous run of a matrix's elements

@@ -4,7 +4,9 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <map>
+#include <string>
 #include <stdexcept>
 #include <utility>
 
@@ -69,55 +71,111 @@ void build_plan(Plan &p) {
       throw std::domain_error("matrix has more than 2^31 - 1 elements");
     groups[{d.P, d.Q}]++;
     p.paper_flops += p.iters * (4.0 * P * P * Q + 2.0 * P * P * P);
-    const double pp = d.Pp, qp = d.Qp;
-    for (int t = 0; t < p.iters; ++t)
-      p.mfma_flops += 4.0 * pp * pp * qp + (p.coeffs[3 * t + 2] != 0.0 ? 2.0 * pp * pp * pp : 0.0);
     p.weight_bytes += double(r) * c * p.elem_bytes();
   }
   p.groups = int32_t(groups.size());
 
-  // matrix order for the GEMM tile lists: largest reduction length first, so
-  // the longest tiles start first (LPT); a matrix's tiles stay contiguous
-  std::vector<int> order;
+  std::vector<int> order;                 // non-empty matrices
   for (int i = 0; i < p.n; ++i)
     if (!p.mats[i].empty) order.push_back(i);
-  std::vector<int> by_q = order, by_p = order;
-  std::stable_sort(by_q.begin(), by_q.end(), [&](int a, int b) {
-    return std::make_pair(p.mats[a].Qp, p.mats[a].Pp) > std::make_pair(p.mats[b].Qp, p.mats[b].Pp);
-  });
-  std::stable_sort(by_p.begin(), by_p.end(), [&](int a, int b) {
-    return std::make_pair(p.mats[a].Pp, p.mats[a].Qp) > std::make_pair(p.mats[b].Pp, p.mats[b].Qp);
-  });
-  p.tiles_pp.clear();
-  for (int i : by_q) {
-    const MatDesc &d = p.mats[i];
-    for (int tm = 0; tm < d.Pp / kTile; ++tm)
-      for (int tn = 0; tn < d.Pp / kTile; ++tn) p.tiles_pp.push_back({i, tm, tn, 0});
+  // Tile class per matrix: the 256 x 256 block tile halves the operand
+  // traffic per flop of the 128 x 128 one and needs 256-aligned padded dims.
+  auto upd_cfg = [&](const MatDesc &d) {
+    return (d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0) ? kCfg256 : kCfg128;
+  };
+  auto pp_cfg = [&](const MatDesc &d) {
+    const char *e = std::getenv("SLORR_GRAM_TILE");
+    const bool big = e && std::string(e) == "256";
+    return (big && d.Pp % kBigTile == 0) ? kCfg256 : kCfg128;
+  };
+  auto tsize = [](int cfg) { return cfg == kCfg256 ? kBigTile : kTile; };
+  p.tiles.clear();
+
+  // XCD-aware order. Workgroup b of a launch runs on XCD b % kXcds, so list
+  // entry b is taken from XCD (b % kXcds)'s own sequence: every matrix's tiles
+  // stay on one XCD (its operand panels are fetched into one L2), matrices are
+  // spread over the XCDs by longest-processing-time on their MFMA work, and
+  // each XCD runs its longest tiles first. Short sequences are padded with
+  // empty tiles (mat = -1), which exit at once.
+  struct Job {
+    int mat;
+    double cost;                 // per tile (proportional to its k extent)
+    std::vector<Tile> tiles;
+  };
+  auto emit = [&](std::vector<Job> jobs) {
+    TileRange r;
+    r.first = int32_t(p.tiles.size());
+    if (jobs.empty()) return r;
+    std::stable_sort(jobs.begin(), jobs.end(), [](const Job &a, const Job &b) {
+      return a.cost * a.tiles.size() > b.cost * b.tiles.size();
+    });
+    std::vector<std::vector<const Job *>> bins(kXcds);
+    std::vector<double> load(kXcds, 0.0);
+    for (const Job &j : jobs) {
+      const int x = int(std::min_element(load.begin(), load.end()) - load.begin());
+      bins[x].push_back(&j);
+      load[x] += j.cost * j.tiles.size();
+    }
+    std::vector<std::vector<Tile>> seq(kXcds);
+    size_t longest = 0;
+    for (int x = 0; x < kXcds; ++x) {
+      std::stable_sort(bins[x].begin(), bins[x].end(),
+                       [](const Job *a, const Job *b) { return a->cost > b->cost; });
+      for (const Job *j : bins[x]) seq[x].insert(seq[x].end(), j->tiles.begin(), j->tiles.end());
+      longest = std::max(longest, seq[x].size());
+    }
+    for (size_t i = 0; i < longest; ++i)
+      for (int x = 0; x < kXcds; ++x)
+        p.tiles.push_back(i < seq[x].size() ? seq[x][i] : Tile{-1, 0, 0, 0});
+    r.count = int32_t(p.tiles.size()) - r.first;
+    return r;
+  };
+  // Gram and Poly outputs are symmetric: upper-triangle tiles only (the
+  // kernel also stores the transpose of off-diagonal tiles)
+  for (int cfg = 0; cfg < 2; ++cfg) {
+    std::vector<Job> jobs;
+    for (int i : order) {
+      const MatDesc &d = p.mats[i];
+      if (pp_cfg(d) != cfg) continue;
+      Job j{i, double(d.Qp) + d.Pp, {}};
+      const int nt = d.Pp / tsize(cfg);
+      for (int tm = 0; tm < nt; ++tm)
+        for (int tn = tm; tn < nt; ++tn) j.tiles.push_back({i, tm, tn, 0});
+      jobs.push_back(std::move(j));
+    }
+    p.pp[cfg] = emit(std::move(jobs));
   }
-  p.tiles_pq.clear();
-  for (int i : by_p) {
-    MatDesc &d = p.mats[i];
-    d.trace_begin = int32_t(p.tiles_pq.size());
-    for (int tm = 0; tm < d.Pp / kTile; ++tm)
-      for (int tn = 0; tn < d.Qp / kTile; ++tn) {
-        const int32_t slot = int32_t(p.tiles_pq.size());
-        p.tiles_pq.push_back({i, tm, tn, slot});
-      }
-    d.trace_end = int32_t(p.tiles_pq.size());
+  // Update tiles; each owns one trace-partial slot, contiguous per matrix
+  int32_t slot = 0;
+  for (int cfg = 0; cfg < 2; ++cfg) {
+    std::vector<Job> jobs;
+    for (int i : order) {
+      MatDesc &d = p.mats[i];
+      if (upd_cfg(d) != cfg) continue;
+      Job j{i, double(d.Pp), {}};
+      d.trace_begin = slot;
+      for (int tm = 0; tm < d.Pp / tsize(cfg); ++tm)
+        for (int tn = 0; tn < d.Qp / tsize(cfg); ++tn) j.tiles.push_back({i, tm, tn, slot++});
+      d.trace_end = slot;
+      jobs.push_back(std::move(j));
+    }
+    p.pq[cfg] = emit(std::move(jobs));
   }
-  p.tiles_prep.clear();
+  p.trace_slots = slot;
   p.chunks.clear();
+  p.prep.first = int32_t(p.tiles.size());
   for (int i = 0; i < p.n; ++i) {
     MatDesc &d = p.mats[i];
     if (d.empty) continue;
     for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
-      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles_prep.push_back({i, tm, tn, 0});
+      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back({i, tm, tn, 0});
     const int64_t total = int64_t(d.rows) * d.cols;
     d.chunk_begin = int32_t(p.chunks.size());
     for (int64_t b = 0; b < total; b += kChunk)
       p.chunks.push_back({i, int32_t(b), int32_t(std::min<int64_t>(kChunk, total - b)), 0});
     d.chunk_end = int32_t(p.chunks.size());
   }
+  p.prep.count = int32_t(p.tiles.size()) - p.prep.first;
 
   // workspace layout
   size_t off = 0;
@@ -130,13 +188,11 @@ void build_plan(Plan &p) {
   p.off_dyn = take(sizeof(DynDesc) * p.n);
   off = p.off_dyn + sizeof(DynDesc) * p.n;          // call params follow the dyn table
   p.off_call = take(sizeof(CallParams));
-  p.off_tiles_pp = take(sizeof(Tile) * p.tiles_pp.size());
-  p.off_tiles_pq = take(sizeof(Tile) * p.tiles_pq.size());
-  p.off_tiles_prep = take(sizeof(Tile) * p.tiles_prep.size());
+  p.off_tiles = take(sizeof(Tile) * p.tiles.size());
   p.off_chunks = take(sizeof(Chunk) * p.chunks.size());
   p.off_scal = take(sizeof(Scalars) * p.n);
   p.off_sumsq = take(sizeof(double) * p.chunks.size());
-  p.off_trace = take(sizeof(double) * p.tiles_pq.size());
+  p.off_trace = take(sizeof(double) * p.trace_slots);
   p.off_static_end = off;
   const size_t es = p.iter_bytes();
   for (int i = 0; i < p.n; ++i) {
@@ -147,35 +203,70 @@ void build_plan(Plan &p) {
     d.x1 = take(pq);
     d.a = take(pp);
     d.b = any_quintic ? take(pp) : d.a;
-    d.pbuf = (p.flags & SLORR_VALUES_ONLY) ? 0 : take(size_t(d.rows) * d.cols * sizeof(float));
   }
   p.ws_bytes = off;
 
   // launch schedule
   p.launches.clear();
-  auto grid_of = [](size_t k) { return int32_t(k); };
-  if (!p.chunks.empty()) p.launches.push_back({Op::SumSq, grid_of(p.chunks.size()), 0, 0, 0, 0, 0});
-  if (p.n > 0) p.launches.push_back({Op::NormFin, (p.n + kThreads - 1) / kThreads, 0, 0, 0, 0, 0});
-  if (!p.tiles_prep.empty()) p.launches.push_back({Op::Prep, grid_of(p.tiles_prep.size()), 2, 0, 0, 0, 0});
-  if (!p.tiles_pp.empty()) {
-    for (int t = 0; t < p.iters; ++t) {
-      const double a = p.coeffs[3 * t], b = p.coeffs[3 * t + 1], c = p.coeffs[3 * t + 2];
-      const int32_t wx = t & 1;
-      // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
-      p.launches.push_back({Op::Gram, grid_of(p.tiles_pp.size()), 0, wx, 0, float(sa / (double(sx) * sx)), 0.0f});
-      const bool quintic = c != 0.0;
-      if (quintic)  // B_s = s_b (b A + c A A) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2)
-        p.launches.push_back({Op::Poly, grid_of(p.tiles_pp.size()), 0, wx, 0,
-                              float(double(sb) * c / (double(sa) * sa)), float(double(sb) * b / sa)});
-      // X'_s = a X_s + (B_s X_s) / s_b      or  a X_s + b (A_s X_s) / s_a  (cubic step)
-      const float alpha = quintic ? float(1.0 / sb) : float(b / sa);
-      const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
-      p.launches.push_back({op, grid_of(p.tiles_pq.size()), 1, wx, quintic ? 0 : 1, alpha, float(a)});
+  auto plain = [](Op op, int32_t grid, int32_t first = 0) {
+    Launch l{};
+    l.op = op;
+    l.grid = grid;
+    l.tile_first = first;
+    return l;
+  };
+  if (!p.chunks.empty()) p.launches.push_back(plain(Op::SumSq, int32_t(p.chunks.size())));
+  if (p.n > 0) p.launches.push_back(plain(Op::NormFin, (p.n + kThreads - 1) / kThreads));
+  if (p.prep.count) p.launches.push_back(plain(Op::Prep, p.prep.count, p.prep.first));
+  auto gemm = [&](Op op, const TileRange &r, int cfg, int32_t wx, int32_t use_a, float alpha, float beta) {
+    if (!r.count) return;
+    Launch l{};
+    l.op = op;
+    l.grid = r.count;
+    l.tile_first = r.first;
+    l.cfg = cfg;
+    l.which_x = wx;
+    l.use_a = use_a;
+    l.alpha = alpha;
+    l.beta = beta;
+    p.launches.push_back(l);
+  };
+  for (int t = 0; t < p.iters; ++t) {
+    const double a = p.coeffs[3 * t], b = p.coeffs[3 * t + 1], c = p.coeffs[3 * t + 2];
+    const int32_t wx = t & 1;
+    const bool quintic = c != 0.0;
+    // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
+    for (int cfg = 1; cfg >= 0; --cfg)
+      gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, float(sa / (double(sx) * sx)), 0.0f);
+    // B_s = s_b (b A + c A A) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2)
+    if (quintic)
+      for (int cfg = 1; cfg >= 0; --cfg)
+        gemm(Op::Poly, p.pp[cfg], cfg, wx, 0, float(double(sb) * c / (double(sa) * sa)),
+             float(double(sb) * b / sa));
+    // X'_s = a X_s + (B_s X_s) / s_b      or  a X_s + b (A_s X_s) / s_a  (cubic step)
+    const float alpha = quintic ? float(1.0 / sb) : float(b / sa);
+    const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
+    for (int cfg = 1; cfg >= 0; --cfg) gemm(op, p.pq[cfg], cfg, wx, quintic ? 0 : 1, alpha, float(a));
+  }
+  p.launches.push_back(plain(Op::Finalize, 1));
+  if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {
+    Launch l = plain(Op::Grad, p.prep.count, p.prep.first);
+    l.which_x = p.iters & 1;                  // buffer the last update wrote
+    p.launches.push_back(l);
+  }
+
+  // MFMA work the launches execute (padded, symmetric tiles counted once)
+  p.mfma_flops = 0;
+  for (const Launch &l : p.launches) {
+    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last) continue;
+    const double ts = tsize(l.cfg);
+    for (int k = 0; k < l.grid; ++k) {
+      const int mi = p.tiles[l.tile_first + k].mat;
+      if (mi < 0) continue;
+      const MatDesc &d = p.mats[mi];
+      p.mfma_flops += 2.0 * ts * ts * (l.op == Op::Gram ? d.Qp : d.Pp);
     }
   }
-  p.launches.push_back({Op::Finalize, 1, 0, 0, 0, 0, 0});
-  if (!(p.flags & SLORR_VALUES_ONLY) && !p.chunks.empty())
-    p.launches.push_back({Op::Grad, grid_of(p.chunks.size()), 0, 0, 0, 0, 0});
 }
 
 }  // namespace slorr

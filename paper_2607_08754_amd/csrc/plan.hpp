@@ -27,13 +27,24 @@ enum class Op : int {
   Grad = SLORR_OP_GRAD           // grad = c1 P - c2 W   (original orientation)
 };
 
+// GEMM block-tile configurations (kernel template instances).
+enum GemmCfg : int32_t {
+  kCfg128 = 0,   // 128 x 128 block tile, 4 waves of 64 x 64
+  kCfg256 = 1    // 256 x 256 block tile, 8 waves of 128 x 64
+};
+
 struct Launch {
   Op op;
   int32_t grid;        // blocks
-  int32_t list;        // which tile list (0: gram/poly, 1: update, 2: prep)
+  int32_t tile_first;  // first entry of the launch's tile list (GEMM, prep)
+  int32_t cfg;         // GemmCfg of a GEMM launch
   int32_t which_x;     // current X buffer (0: x0, 1: x1)
   int32_t use_a;       // update operand is A (cubic step) instead of B
   float alpha, beta;   // epilogue coefficients
+};
+
+struct TileRange {
+  int32_t first = 0, count = 0;
 };
 
 struct Plan {
@@ -50,16 +61,17 @@ struct Plan {
   // derived
   int32_t groups = 0;
   std::vector<MatDesc> mats;
-  std::vector<Tile> tiles_pp;          // P x P outputs (gram, poly)
-  std::vector<Tile> tiles_pq;          // P x Q outputs (update, last)
-  std::vector<Tile> tiles_prep;        // prep tiles over Pp x Qp
+  std::vector<Tile> tiles;             // all tile lists, concatenated
+  TileRange pp[2];                     // P x P outputs (gram, poly), per GemmCfg
+  TileRange pq[2];                     // P x Q outputs (update, last), per GemmCfg
+  TileRange prep;                      // prep tiles over Pp x Qp
+  int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
   std::vector<Launch> launches;
   double paper_flops = 0, mfma_flops = 0, weight_bytes = 0;
   // workspace layout (byte offsets)
-  size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles_pp = 0, off_tiles_pq = 0,
-         off_tiles_prep = 0, off_chunks = 0, off_scal = 0, off_sumsq = 0, off_trace = 0,
-         off_static_end = 0, ws_bytes = 0;
+  size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles = 0, off_chunks = 0, off_scal = 0,
+         off_sumsq = 0, off_trace = 0, off_static_end = 0, ws_bytes = 0;
   // runtime state (owned by the API layer)
   void *ws = nullptr;
   int device = -1;
