@@ -50,6 +50,11 @@ def build(verbose: bool = False) -> str:
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}\n{res.stderr}")
+    # a kernel whose host stub went missing would only fail at dlopen time
+    und = subprocess.run(["nm", "-u", "--demangle", tmp], capture_output=True, text=True).stdout
+    bad = [l for l in und.splitlines() if "slorr" in l]
+    if bad:
+        raise RuntimeError("undefined library symbols:\n" + "\n".join(bad))
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

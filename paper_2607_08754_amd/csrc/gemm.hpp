@@ -3,11 +3,14 @@
 // one output tile from the launch's tile list.
 //
 //   Gram    A  = X X^T                 NT: both operands are rows of X (k = Q)
-//   Poly    B  = b A + c A A^T         NT on the symmetric A (A A^T = A A)
-//   Update  X' = a X + B X             B symmetric (rows of B = columns of B);
+//   Poly    B  = b A + c A A^T + a I   NT on the symmetric A (A A^T = A A); the
+//                                      a X term of the step is folded into B
+//   Update  X' = B X                   B symmetric (rows of B = columns of B);
 //                                      X is read as [k][n] and transposed into
-//                                      the K-major LDS layout on the way in
-//   Last    X_T = a X + B X, stored like an update, with the per-tile partial
+//                                      the K-major LDS layout on the way in.
+//                                      Cubic steps (no Poly) use X' = a X + b A X
+//                                      with the a X term in the epilogue.
+//   Last    X_T = B X, stored like an update, with the per-tile partial
 //           sums of W * P (P = X_T in fp32; the trace of W^T P) read against W
 //           in its own orientation
 //
@@ -21,8 +24,8 @@
 // stores of the NK loader (8 lanes per row) and of the transposing KN loader
 // (16 lanes per row, 8-byte pieces) are conflict-free too.
 //
-// Pipeline: two LDS stages, one barrier per k-slab; the global loads of slab
-// k+1 are in flight while the MFMAs of slab k run.
+// Pipeline: two LDS stages and two register sets, one barrier per k-slab;
+// the global loads of slab k+2 are in flight while the MFMAs of slab k run.
 // Included inside namespace slorr, after the helpers of kernels.hip.
 #pragma once
 
@@ -60,7 +63,8 @@ struct GemmArgs {
   int which_x;    // current X buffer
   int use_a;      // update operand is A (cubic step)
   int write_x;    // Last: store X_T (the gradient kernel reads it)
-  float alpha, beta, inv_sx;
+  int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
+  float alpha, beta, gamma, inv_sx;
 };
 
 template <int BM, int BN, int WGM, int WGN>
@@ -83,6 +87,19 @@ struct GemmShape {
 // distinct positions per parity.
 __device__ __forceinline__ int swz_key(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ swz_key(row)) << 4); }
+
+// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
+// at lds_base + 16 l (lds_base wave-uniform, passed in m0). Device pass only:
+// the host pass of the single-source build just needs the kernel's stub.
+__device__ __forceinline__ void load_lds16(const void *g, void *lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((address_space(3))) void lds_void;
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)lds_base, 16, 0, 0);
+#else
+  (void)g;
+  (void)lds_base;
+#endif
+}
 
 // sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
 template <typename Tw>
@@ -150,8 +167,9 @@ __device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
   }
 }
 
-template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
+template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN, int DEPTH>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
+  static_assert(DEPTH == 1 || DEPTH == 2, "prefetch depth");
   using S = GemmShape<BM, BN, WGM, WGN>;
   constexpr int NT = S::kThreads;
   constexpr int V = Mfma<T>::V;
@@ -193,20 +211,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const int lr = lane & 31, lk = lane >> 5;
   const int wm = wave / WGN, wn = wave % WGN;
 
-  frag ra[CA];
-  frag rb[KN ? 4 * QB : CB];
+  // two register sets: slab k + 2 is loaded while slab k is multiplied and
+  // slab k + 1 waits in the other set
+  frag ra[DEPTH][CA];
+  frag rb[DEPTH][KN ? 4 * QB : CB];
 
-  auto gload = [&](int k0) {
+  auto gload = [&](auto set_c, int k0) {
+    constexpr int set = decltype(set_c)::value;
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
       const int q = tid + i * NT, row = q >> 3, c = q & 7;
-      ra[i] = *reinterpret_cast<const frag *>(Ap + size_t(m0 + row) * lda + k0 + c * V);
+      ra[set][i] = *reinterpret_cast<const frag *>(Ap + size_t(m0 + row) * lda + k0 + c * V);
     }
     if constexpr (!KN) {
 #pragma unroll
       for (int i = 0; i < CB; ++i) {
         const int q = tid + i * NT, row = q >> 3, c = q & 7;
-        rb[i] = *reinterpret_cast<const frag *>(Bp + size_t(n0 + row) * ldb + k0 + c * V);
+        rb[set][i] = *reinterpret_cast<const frag *>(Bp + size_t(n0 + row) * ldb + k0 + c * V);
       }
     } else {
 #pragma unroll
@@ -214,23 +235,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          rb[4 * i + r] = *reinterpret_cast<const frag *>(Bp + size_t(k0 + 4 * kq + r) * ldb + n0 + nc * V);
+          rb[set][4 * i + r] =
+              *reinterpret_cast<const frag *>(Bp + size_t(k0 + 4 * kq + r) * ldb + n0 + nc * V);
       }
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](auto set_c, int buf) {
+    constexpr int set = decltype(set_c)::value;
     char *sA = smem + buf * S::kStage;
     char *sB = sA + BM * 128;
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
       const int q = tid + i * NT, row = q >> 3, c = q & 7;
-      *reinterpret_cast<frag *>(sA + swz(row, c)) = ra[i];
+      *reinterpret_cast<frag *>(sA + swz(row, c)) = ra[set][i];
     }
     if constexpr (!KN) {
 #pragma unroll
       for (int i = 0; i < CB; ++i) {
         const int q = tid + i * NT, row = q >> 3, c = q & 7;
-        *reinterpret_cast<frag *>(sB + swz(row, c)) = rb[i];
+        *reinterpret_cast<frag *>(sB + swz(row, c)) = rb[set][i];
       }
     } else {
 #pragma unroll
@@ -241,10 +264,66 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         for (int j = 0; j < V; ++j) {
           const int n = nc * V + j;
           quad_t v;
-          v[0] = rb[4 * i + 0][j];
-          v[1] = rb[4 * i + 1][j];
-          v[2] = rb[4 * i + 2][j];
-          v[3] = rb[4 * i + 3][j];
+          v[0] = rb[set][4 * i + 0][j];
+          v[1] = rb[set][4 * i + 1][j];
+          v[2] = rb[set][4 * i + 2][j];
+          v[3] = rb[set][4 * i + 3][j];
+          *reinterpret_cast<quad_t *>(sB + swz(n, byte >> 4) + (byte & 15)) = v;
+        }
+      }
+    }
+  };
+
+  // Direct global -> LDS loads (global_load_lds_dwordx4) of the K-major
+  // operands: one wave instruction fills 8 consecutive LDS rows (1 KB) at the
+  // wave-uniform base in m0, lane l landing at base + 16 l, i.e. row l / 8,
+  // physical chunk l % 8; the lane therefore fetches logical chunk
+  // (l % 8) ^ key(row). No registers, no ds_write instructions.
+  auto dload = [&](int k0, int buf) {
+    char *sA = smem + buf * S::kStage;
+    char *sB = sA + BM * 128;
+    const int rsub = lane >> 3, pch = lane & 7;
+#pragma unroll
+    for (int i = 0; i < BM / 8 / S::kWaves; ++i) {
+      const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
+      load_lds16(Ap + size_t(m0 + row) * lda + k0 + (pch ^ swz_key(row)) * V, sA + r0 * 128);
+    }
+    if constexpr (!KN) {
+#pragma unroll
+      for (int i = 0; i < BN / 8 / S::kWaves; ++i) {
+        const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
+        load_lds16(Bp + size_t(n0 + row) * ldb + k0 + (pch ^ swz_key(row)) * V, sB + r0 * 128);
+      }
+    }
+  };
+  // the transposing loader of the [k][n] operand (update) into registers
+  frag rk[KN ? 4 * QB : 1];
+  auto kload = [&](int k0) {
+    if constexpr (KN) {
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          rk[4 * i + r] = *reinterpret_cast<const frag *>(Bp + size_t(k0 + 4 * kq + r) * ldb + n0 + nc * V);
+      }
+    }
+  };
+  auto kstore = [&](int buf) {
+    if constexpr (KN) {
+      char *sB = smem + buf * S::kStage + BM * 128;
+#pragma unroll
+      for (int i = 0; i < QB; ++i) {
+        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
+        const int byte = 4 * kq * int(sizeof(T));
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const int n = nc * V + j;
+          quad_t v;
+          v[0] = rk[4 * i + 0][j];
+          v[1] = rk[4 * i + 1][j];
+          v[2] = rk[4 * i + 2][j];
+          v[3] = rk[4 * i + 3][j];
           *reinterpret_cast<quad_t *>(sB + swz(n, byte >> 4) + (byte & 15)) = v;
         }
       }
@@ -259,34 +338,68 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s run
   auto compute = [&](int buf) {
     const char *sA = smem + buf * S::kStage;
     const char *sB = sA + BM * 128;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      frag fa[FM], fb[FN];
+    frag fa[2][FM], fb[2][FN];
+    auto read = [&](int s, int slot) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        fa[i] = *reinterpret_cast<const frag *>(sA + swz(wm * WTM + i * 32 + lr, 2 * s + lk));
+        fa[slot][i] = *reinterpret_cast<const frag *>(sA + swz(wm * WTM + i * 32 + lr, 2 * s + lk));
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        fb[j] = *reinterpret_cast<const frag *>(sB + swz(wn * WTN + j * 32 + lr, 2 * s + lk));
+        fb[slot][j] = *reinterpret_cast<const frag *>(sB + swz(wn * WTN + j * 32 + lr, 2 * s + lk));
+    };
+    read(0, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (s < 3) read(s + 1, (s + 1) & 1);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Mfma<T>::mma(acc[i][j], fa[i], fb[j]);
+        for (int j = 0; j < FN; ++j) Mfma<T>::mma(acc[i][j], fa[s & 1][i], fb[s & 1][j]);
     }
   };
 
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, DEPTH - 1>;
+  // K is a multiple of 128 (padding), BK divides 64, so the slab count is even
   const int nk = K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    compute(kt & 1);
-    if (kt + 1 < nk) sstore((kt + 1) & 1);
+  if constexpr (DEPTH == 2) {
+    gload(S0{}, 0);
+    gload(S1{}, BK);
+    sstore(S0{}, 0);
     __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      // LDS stage 0 holds slab kt, set 1 slab kt + 1, set 0 is free
+      if (kt + 2 < nk) gload(S0{}, (kt + 2) * BK);
+      compute(0);
+      sstore(S1{}, 1);
+      __syncthreads();
+      // LDS stage 1 holds slab kt + 1, set 0 slab kt + 2, set 1 is free
+      if (kt + 3 < nk) gload(S1{}, (kt + 3) * BK);
+      compute(1);
+      if (kt + 2 < nk) sstore(S0{}, 0);
+      __syncthreads();
+    }
+  } else {
+    // one LDS stage in use, the other being filled by direct loads (and the
+    // transposed update operand) for the next slab
+    dload(0, 0);
+    kload(0);
+    kstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int nb = (kt + 1) & 1;
+      if (kt + 1 < nk) {
+        dload((kt + 1) * BK, nb);
+        kload((kt + 1) * BK);
+      }
+      compute(kt & 1);
+      if (kt + 1 < nk) kstore(nb);
+      __syncthreads();
+    }
   }
 
   // ------------------------------------------------------------ epilogue
@@ -332,13 +445,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         float in[8];
         load8(Am + size_t(grow) * d.Pp + gcol, in);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
+        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
         store8(Bm + size_t(grow) * d.Pp + gcol, v);
       } else {
-        float in[8];
-        load8(Xc + size_t(grow) * d.Qp + gcol, in);
+        if (args.fold) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
+          for (int j = 0; j < 8; ++j) v[j] *= alpha;
+        } else {
+          float in[8];
+          load8(Xc + size_t(grow) * d.Qp + gcol, in);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
+        }
         if (MODE == kUpdate || args.write_x) store8(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
 #pragma unroll

@@ -8,8 +8,8 @@
 //              factor"; App. D remark on normalisation)
 //   k_gemm     the Polar Express step (Sec. 3; App. E.1) as three MFMA GEMMs:
 //                Gram    A = X X^T
-//                Poly    B = b A + c A A            (A symmetric: A A = A A^T)
-//                Update  X' = a X + B X             (B symmetric)
+//                Poly    B = b A + c A A + a I      (A symmetric: A A = A A^T)
+//                Update  X' = B X                   (B symmetric)
 //                Last    X_T = a X + B X with the trace partials of
 //                        sum(W * P), P = X_T (Sec. 3 "Computing the nuclear
 //                        and Frobenius norms")
@@ -20,8 +20,10 @@
 //              caller's buffer (App. E.3)
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
 #include <stdexcept>
 #include <string>
+#include <type_traits>
 
 #include "kernels.hpp"
 #include "layout.hpp"
@@ -60,6 +62,68 @@ __device__ __forceinline__ double block_sum(double v, double *sh) {
   return r;
 }
 
+// Sum over the 64 lanes of a wave: butterfly in a fixed order (bitwise
+// reproducible); every lane ends with the total.
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Up to 8 consecutive elements at p (n of them valid) as floats; one vector
+// access when all 8 are valid and p is 16-byte aligned.
+template <typename T>
+__device__ __forceinline__ void get8(const T *p, int n, float (&v)[8]) {
+  if (n >= 8 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    if constexpr (sizeof(T) == 2) {
+      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+      const u16x8 h = *reinterpret_cast<const u16x8 *>(p);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        uint16_t b = h[j];
+        v[j] = to_f(*reinterpret_cast<const T *>(&b));
+      }
+    } else {
+      const float4v a = reinterpret_cast<const float4v *>(p)[0];
+      const float4v b = reinterpret_cast<const float4v *>(p)[1];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[j] = a[j];
+        v[4 + j] = b[j];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = j < n ? to_f(p[j]) : 0.0f;
+  }
+}
+
+// Up to 8 consecutive values to p (n of them), vector stores when possible.
+template <typename T>
+__device__ __forceinline__ void put8(T *p, int n, const float (&v)[8]) {
+  if (n >= 8 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    if constexpr (sizeof(T) == 2) {
+      half8 h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) h[j] = _Float16(v[j]);
+      *reinterpret_cast<half8 *>(p) = h;
+    } else {
+      float4v a, b;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[j] = v[j];
+        b[j] = v[4 + j];
+      }
+      reinterpret_cast<float4v *>(p)[0] = a;
+      reinterpret_cast<float4v *>(p)[1] = b;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (j < n) p[j] = from_f<T>(v[j]);
+  }
+}
+
 // --------------------------------------------------------------- reductions
 
 template <typename Tw>
@@ -89,23 +153,33 @@ __global__ __launch_bounds__(kThreads) void k_sumsq(const Chunk *__restrict__ ch
   if (threadIdx.x == 0) part[blockIdx.x] = r;
 }
 
+// f and f + eps per matrix: one wave per matrix sums its chunk partials
+// (lane-strided, then a fixed butterfly).
 __global__ __launch_bounds__(kThreads) void k_norm_fin(const MatDesc *__restrict__ mats,
                                                        Scalars *__restrict__ sc,
                                                        const double *__restrict__ part, int n,
                                                        float eps) {
-  const int i = blockIdx.x * kThreads + threadIdx.x;
+  const int i = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (i >= n) return;
   const MatDesc d = mats[i];
   double s = 0.0;
-  for (int c = d.chunk_begin; c < d.chunk_end; ++c) s += part[c];
-  const double f = sqrt(s), fe = f + double(eps);
-  sc[i].sumsq = s;
-  sc[i].f = f;
-  sc[i].feps = fe;
-  sc[i].inv_feps = fe > 0.0 ? float(1.0 / fe) : 0.0f;
+  for (int c = d.chunk_begin + lane; c < d.chunk_end; c += 64) s += part[c];
+  s = wave_sum(s);
+  if (lane == 0) {
+    const double f = sqrt(s), fe = f + double(eps);
+    sc[i].sumsq = s;
+    sc[i].f = f;
+    sc[i].feps = fe;
+    sc[i].inv_feps = fe > 0.0 ? float(1.0 / fe) : 0.0f;
+  }
 }
 
 // ---------------------------------------------------------------- normalise
+
+// 64 x 64 canonical tile per block. Rows of W are read 8 elements at a time
+// (vector when aligned), staged in LDS as fp32, and written 8 at a time
+// along the canonical rows (transposed for tall W).
+constexpr int kPrepPitch = kPrepTile + 4;
 
 template <typename Tw, typename Tx>
 __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tiles,
@@ -113,31 +187,31 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
                                                    const DynDesc *__restrict__ dyn,
                                                    const Scalars *__restrict__ sc, char *ws,
                                                    float sx) {
-  __shared__ float tile[kPrepTile][kPrepTile + 1];
+  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
   const Tile t = tiles[blockIdx.x];
   const MatDesc d = mats[t.mat];
   const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
   const float scale = sc[t.mat].inv_feps * sx;
   Tx *x = reinterpret_cast<Tx *>(ws + d.x0);
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
-  // source block in W's own row-major order (coalesced reads)
-  for (int i = threadIdx.x; i < kPrepTile * kPrepTile; i += kThreads) {
-    const int r = i / kPrepTile, c = i % kPrepTile;
-    float v = 0.0f;
-    if (!d.tall) {
-      const int m = m0 + r, nn = n0 + c;
-      if (m < d.P && nn < d.Q) v = to_f(w[size_t(m) * d.cols + nn]);
-    } else {
-      const int nn = n0 + r, m = m0 + c;
-      if (nn < d.Q && m < d.P) v = to_f(w[size_t(nn) * d.cols + m]);
-    }
-    tile[r][c] = v * scale;
+  // source rows of W covered by the tile: wide -> canonical rows m, tall -> canonical columns n
+  const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;
+  const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+    float v[8];
+    const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
+    get8(w + size_t(r0 + r) * d.cols + c0 + c, nv, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j] * scale;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < kPrepTile * kPrepTile; i += kThreads) {
-    const int r = i / kPrepTile, c = i % kPrepTile;
-    const float v = d.tall ? tile[c][r] : tile[r][c];
-    x[size_t(m0 + r) * d.Qp + n0 + c] = from_f<Tx>(v);
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;   // canonical (m0 + r, n0 + c..)
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = d.tall ? tile[(c + j) * kPrepPitch + r] : tile[r * kPrepPitch + c + j];
+    put8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
   }
 }
 
@@ -147,6 +221,9 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
 
 // ---------------------------------------------------------------- finalize
 
+// Values and gradient factors; one wave per matrix reduces its trace
+// partials (lane-strided, fixed butterfly). One block; the set sum is taken
+// by thread 0 in index order.
 __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict__ mats,
                                                        Scalars *sc,
                                                        const double *__restrict__ tpart,
@@ -154,10 +231,13 @@ __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict
                                                        int n, int kind, int aux) {
   float *out = call->out_vals;
   const double g = double(call->grad_scale);
-  for (int i = threadIdx.x; i < n; i += kThreads) {
+  const int lane = threadIdx.x & 63;
+  for (int i = threadIdx.x >> 6; i < n; i += kThreads / 64) {
     const MatDesc d = mats[i];
     double nh = 0.0;
-    for (int s = d.trace_begin; s < d.trace_end; ++s) nh += tpart[s];
+    for (int s = d.trace_begin + lane; s < d.trace_end; s += 64) nh += tpart[s];
+    nh = wave_sum(nh);
+    if (lane != 0) continue;
     const double fe = d.empty ? 0.0 : sc[i].feps;
     double L = 0.0, c1 = 0.0, c2 = 0.0;
     if (d.empty || fe == 0.0) {
@@ -194,8 +274,9 @@ __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict
 
 // Gradient in W's own orientation from the last iterate X_T (canonical,
 // zero-padded, scale s_x): grad = c1 X_T / s_x - c2 W (+ grad). One block per
-// 64 x 64 canonical tile; tall matrices are transposed through LDS so that
-// both the reads of W / grad and the writes of grad run along W's rows.
+// 64 x 64 canonical tile: X_T rows are read 8 at a time, staged in LDS (fp32)
+// and read back along W's rows (transposed for tall W), so that W and grad
+// are accessed 8 consecutive elements at a time.
 template <typename Tw, typename Tx>
 __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tiles,
                                                    const MatDesc *__restrict__ mats,
@@ -203,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
                                                    const Scalars *__restrict__ sc,
                                                    const char *__restrict__ ws, int xsel, float inv_sx,
                                                    int accumulate) {
-  __shared__ float tile[kPrepTile][kPrepTile + 1];
+  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
   const Tile t = tiles[blockIdx.x];
   const MatDesc d = mats[t.mat];
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
@@ -212,30 +293,35 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
   float *g = dyn[t.mat].g;
   const float c1 = float(sc[t.mat].c1) * inv_sx, c2 = float(sc[t.mat].c2);
-  for (int i = threadIdx.x; i < kPrepTile * kPrepTile; i += kThreads) {
-    const int r = i / kPrepTile, c = i % kPrepTile;
-    tile[r][c] = to_f(x[size_t(m0 + r) * d.Qp + n0 + c]);
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+    float v[8];
+    get8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j];
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < kPrepTile * kPrepTile; i += kThreads) {
-    const int r = i / kPrepTile, c = i % kPrepTile;
-    int m, n;
-    float p;
-    if (!d.tall) {
-      m = m0 + r;
-      n = n0 + c;
-      p = tile[r][c];
-    } else {            // W row n0 + r, column m0 + c
-      m = m0 + c;
-      n = n0 + r;
-      p = tile[c][r];
+  const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;     // rows / columns of W
+  const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+    if (r0 + r >= rlim || c0 + c >= clim) continue;
+    const int nv = min(8, clim - (c0 + c));
+    const size_t o = size_t(r0 + r) * d.cols + c0 + c;
+    float wv[8], v[8];
+    get8(w + o, nv, wv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float p = d.tall ? tile[(c + j) * kPrepPitch + r] : tile[r * kPrepPitch + c + j];
+      v[j] = c1 * p - c2 * wv[j];
     }
-    if (m < d.P && n < d.Q) {
-      const size_t o = d.tall ? size_t(n) * d.cols + m : size_t(m) * d.cols + n;
-      float v = c1 * p - c2 * to_f(w[o]);
-      if (accumulate) v += g[o];
-      g[o] = v;
+    if (accumulate) {
+      float old[8];
+      get8(g + o, nv, old);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] += old[j];
     }
+    put8(g + o, nv, v);
   }
 }
 
@@ -247,21 +333,21 @@ void check(hipError_t e, const char *what) {
   if (e != hipSuccess) throw HipError(std::string(what) + ": " + hipGetErrorString(e));
 }
 
-template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
+template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN, int DEPTH>
 void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
   switch (op) {
     case Op::Gram:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
       break;
     case Op::Poly:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
       break;
     case Op::Update:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
       break;
     default:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
       break;
   }
 }
@@ -288,7 +374,7 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         hipLaunchKernelGGL(k_sumsq<Tw>, grid, block, 0, s, chunks, dyn, sumsq);
         break;
       case Op::NormFin:
-        hipLaunchKernelGGL(k_norm_fin, grid, block, 0, s, mats, sc, sumsq, p.n, p.eps);
+        hipLaunchKernelGGL(k_norm_fin, grid, block, 0, s, mats, sc, sumsq, p.n, p.eps);   // 4 matrices per block
         break;
       case Op::Prep:
         hipLaunchKernelGGL((k_prep<Tw, Tx>), grid, block, 0, s, tiles + l.tile_first, mats, dyn, sc, ws, sx);
@@ -308,11 +394,17 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.write_x = (p.flags & SLORR_VALUES_ONLY) ? 0 : 1;
         a.alpha = l.alpha;
         a.beta = l.beta;
+        a.gamma = l.gamma;
+        a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         if (l.cfg == kCfg256)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 2, 1>(l.op, grid, a, s);
+        else if (l.cfg == kCfg256w8)
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4, 1>(l.op, grid, a, s);
+        else if (std::getenv("SLORR_D128") && std::string(std::getenv("SLORR_D128")) == "2")
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2, 2>(l.op, grid, a, s);
         else
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2, 1>(l.op, grid, a, s);
         break;
       }
       case Op::Finalize:

@@ -81,14 +81,17 @@ void build_plan(Plan &p) {
   // Tile class per matrix: the 256 x 256 block tile halves the operand
   // traffic per flop of the 128 x 128 one and needs 256-aligned padded dims.
   auto upd_cfg = [&](const MatDesc &d) {
-    return (d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0) ? kCfg256 : kCfg128;
+    const char *e = std::getenv("SLORR_UPD_TILE");
+    const std::string v = e ? e : "256w8";
+    if (v == "128" || !(d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0)) return kCfg128;
+    return v == "256w8" ? kCfg256w8 : kCfg256;
   };
   auto pp_cfg = [&](const MatDesc &d) {
     const char *e = std::getenv("SLORR_GRAM_TILE");
     const bool big = e && std::string(e) == "256";
     return (big && d.Pp % kBigTile == 0) ? kCfg256 : kCfg128;
   };
-  auto tsize = [](int cfg) { return cfg == kCfg256 ? kBigTile : kTile; };
+  auto tsize = [](int cfg) { return cfg == kCfg128 ? kTile : kBigTile; };
   p.tiles.clear();
 
   // XCD-aware order. Workgroup b of a launch runs on XCD b % kXcds, so list
@@ -102,10 +105,23 @@ void build_plan(Plan &p) {
     double cost;                 // per tile (proportional to its k extent)
     std::vector<Tile> tiles;
   };
-  auto emit = [&](std::vector<Job> jobs) {
+  auto emit = [&](std::vector<Job> whole) {
     TileRange r;
     r.first = int32_t(p.tiles.size());
-    if (jobs.empty()) return r;
+    if (whole.empty()) return r;
+    // a set of few large matrices would leave XCDs idle: cut every matrix into
+    // jobs of at most 1/16 of the launch's tiles (whole row bands first)
+    size_t total = 0;
+    for (const Job &j : whole) total += j.tiles.size();
+    const size_t cap = std::max<size_t>(1, (total + 2 * kXcds - 1) / (2 * kXcds));
+    std::vector<Job> jobs;
+    for (Job &j : whole) {
+      for (size_t b = 0; b < j.tiles.size(); b += cap) {
+        Job part{j.mat, j.cost, {}};
+        part.tiles.assign(j.tiles.begin() + b, j.tiles.begin() + std::min(j.tiles.size(), b + cap));
+        jobs.push_back(std::move(part));
+      }
+    }
     std::stable_sort(jobs.begin(), jobs.end(), [](const Job &a, const Job &b) {
       return a.cost * a.tiles.size() > b.cost * b.tiles.size();
     });
@@ -132,7 +148,7 @@ void build_plan(Plan &p) {
   };
   // Gram and Poly outputs are symmetric: upper-triangle tiles only (the
   // kernel also stores the transpose of off-diagonal tiles)
-  for (int cfg = 0; cfg < 2; ++cfg) {
+  for (int cfg = 0; cfg < 3; ++cfg) {
     std::vector<Job> jobs;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
@@ -147,7 +163,7 @@ void build_plan(Plan &p) {
   }
   // Update tiles; each owns one trace-partial slot, contiguous per matrix
   int32_t slot = 0;
-  for (int cfg = 0; cfg < 2; ++cfg) {
+  for (int cfg = 0; cfg < 3; ++cfg) {
     std::vector<Job> jobs;
     for (int i : order) {
       MatDesc &d = p.mats[i];
@@ -216,9 +232,10 @@ void build_plan(Plan &p) {
     return l;
   };
   if (!p.chunks.empty()) p.launches.push_back(plain(Op::SumSq, int32_t(p.chunks.size())));
-  if (p.n > 0) p.launches.push_back(plain(Op::NormFin, (p.n + kThreads - 1) / kThreads));
+  if (p.n > 0) p.launches.push_back(plain(Op::NormFin, (p.n + kThreads / 64 - 1) / (kThreads / 64)));
   if (p.prep.count) p.launches.push_back(plain(Op::Prep, p.prep.count, p.prep.first));
-  auto gemm = [&](Op op, const TileRange &r, int cfg, int32_t wx, int32_t use_a, float alpha, float beta) {
+  auto gemm = [&](Op op, const TileRange &r, int cfg, int32_t wx, int32_t use_a, int32_t fold, float alpha,
+                  float beta, float gamma) {
     if (!r.count) return;
     Launch l{};
     l.op = op;
@@ -227,8 +244,10 @@ void build_plan(Plan &p) {
     l.cfg = cfg;
     l.which_x = wx;
     l.use_a = use_a;
+    l.fold = fold;
     l.alpha = alpha;
     l.beta = beta;
+    l.gamma = gamma;
     p.launches.push_back(l);
   };
   for (int t = 0; t < p.iters; ++t) {
@@ -236,17 +255,23 @@ void build_plan(Plan &p) {
     const int32_t wx = t & 1;
     const bool quintic = c != 0.0;
     // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
-    for (int cfg = 1; cfg >= 0; --cfg)
-      gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, float(sa / (double(sx) * sx)), 0.0f);
-    // B_s = s_b (b A + c A A) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2)
-    if (quintic)
-      for (int cfg = 1; cfg >= 0; --cfg)
-        gemm(Op::Poly, p.pp[cfg], cfg, wx, 0, float(double(sb) * c / (double(sa) * sa)),
-             float(double(sb) * b / sa));
-    // X'_s = a X_s + (B_s X_s) / s_b      or  a X_s + b (A_s X_s) / s_a  (cubic step)
-    const float alpha = quintic ? float(1.0 / sb) : float(b / sa);
+    for (int cfg = 2; cfg >= 0; --cfg)
+      gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, 0, float(sa / (double(sx) * sx)), 0.0f, 0.0f);
     const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
-    for (int cfg = 1; cfg >= 0; --cfg) gemm(op, p.pq[cfg], cfg, wx, quintic ? 0 : 1, alpha, float(a));
+    if (quintic) {
+      // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
+      // the step X' = a X + (b A + c A A) X becomes X' = B X
+      for (int cfg = 2; cfg >= 0; --cfg)
+        gemm(Op::Poly, p.pp[cfg], cfg, wx, 0, 0, float(double(sb) * c / (double(sa) * sa)),
+             float(double(sb) * b / sa), float(double(sb) * a));
+      // X'_s = (B_s X_s) / s_b
+      for (int cfg = 2; cfg >= 0; --cfg)
+        gemm(op, p.pq[cfg], cfg, wx, 0, 1, float(1.0 / sb), 0.0f, 0.0f);
+    } else {
+      // cubic step: X'_s = a X_s + b (A_s X_s) / s_a
+      for (int cfg = 2; cfg >= 0; --cfg)
+        gemm(op, p.pq[cfg], cfg, wx, 1, 0, float(b / sa), float(a), 0.0f);
+    }
   }
   p.launches.push_back(plain(Op::Finalize, 1));
   if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {

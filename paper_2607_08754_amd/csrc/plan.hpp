@@ -30,7 +30,8 @@ enum class Op : int {
 // GEMM block-tile configurations (kernel template instances).
 enum GemmCfg : int32_t {
   kCfg128 = 0,   // 128 x 128 block tile, 4 waves of 64 x 64
-  kCfg256 = 1    // 256 x 256 block tile, 8 waves of 128 x 64
+  kCfg256 = 1,   // 256 x 256 block tile, 4 waves of 128 x 128
+  kCfg256w8 = 2  // 256 x 256 block tile, 8 waves of 128 x 64
 };
 
 struct Launch {
@@ -40,7 +41,8 @@ struct Launch {
   int32_t cfg;         // GemmCfg of a GEMM launch
   int32_t which_x;     // current X buffer (0: x0, 1: x1)
   int32_t use_a;       // update operand is A (cubic step) instead of B
-  float alpha, beta;   // epilogue coefficients
+  int32_t fold;        // update: a_t I already folded into B (no a X term)
+  float alpha, beta, gamma;  // epilogue coefficients
 };
 
 struct TileRange {
@@ -62,8 +64,8 @@ struct Plan {
   int32_t groups = 0;
   std::vector<MatDesc> mats;
   std::vector<Tile> tiles;             // all tile lists, concatenated
-  TileRange pp[2];                     // P x P outputs (gram, poly), per GemmCfg
-  TileRange pq[2];                     // P x Q outputs (update, last), per GemmCfg
+  TileRange pp[3];                     // P x P outputs (gram, poly), per GemmCfg
+  TileRange pq[3];                     // P x Q outputs (update, last), per GemmCfg
   TileRange prep;                      // prep tiles over Pp x Qp
   int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
