@@ -41,8 +41,14 @@ def _alg_flops_per_launch(shapes, op):
 
 
 def _kernels_hash():
-    with open(os.path.join(ROOT, "paper_2607_08754_amd", "csrc", "kernels.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the library's sources (kernels and the plan that orders their tiles)."""
+    csrc = os.path.join(ROOT, "paper_2607_08754_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".cpp", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def _traffic(config, op):

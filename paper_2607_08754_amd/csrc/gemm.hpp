@@ -24,8 +24,10 @@
 // stores of the NK loader (8 lanes per row) and of the transposing KN loader
 // (16 lanes per row, 8-byte pieces) are conflict-free too.
 //
-// Pipeline: two LDS stages and two register sets, one barrier per k-slab;
-// the global loads of slab k+2 are in flight while the MFMAs of slab k run.
+// Pipeline: two LDS stages, one barrier per k-slab. The K-major operands go
+// global -> LDS directly (no registers); the [k][n] operand of the update is
+// loaded into registers and stored transposed. The loads of slab k + 1 are in
+// flight while the MFMAs of slab k run.
 // Included inside namespace slorr, after the helpers of kernels.hip.
 #pragma once
 
@@ -167,19 +169,16 @@ __device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
   }
 }
 
-template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN, int DEPTH>
+template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
-  static_assert(DEPTH == 1 || DEPTH == 2, "prefetch depth");
   using S = GemmShape<BM, BN, WGM, WGN>;
   constexpr int NT = S::kThreads;
   constexpr int V = Mfma<T>::V;
   constexpr int BK = 8 * V;                      // k per slab (128-byte rows)
   constexpr int FM = S::FM, FN = S::FN, WTM = S::WTM, WTN = S::WTN;
   constexpr bool KN = (MODE == kUpdate || MODE == kLast);
-  constexpr int CA = BM * 8 / NT;                // 16-byte chunks per thread, A slab
-  constexpr int CB = BN * 8 / NT;                // same, B slab (NK)
   constexpr int QB = (BK / 4) * (BN / V) / NT;   // 4 x V blocks per thread, B slab (KN)
-  static_assert(CA * NT == BM * 8 && CB * NT == BN * 8, "tile / thread mismatch");
+  static_assert(BM % (8 * S::kWaves) == 0 && BN % (8 * S::kWaves) == 0, "tile / wave mismatch");
   static_assert(!KN || QB * NT == (BK / 4) * (BN / V), "KN loader mismatch");
   static_assert(FM >= 1 && FN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   typedef typename Mfma<T>::frag frag;
@@ -210,69 +209,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const int lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
   const int wm = wave / WGN, wn = wave % WGN;
-
-  // two register sets: slab k + 2 is loaded while slab k is multiplied and
-  // slab k + 1 waits in the other set
-  frag ra[DEPTH][CA];
-  frag rb[DEPTH][KN ? 4 * QB : CB];
-
-  auto gload = [&](auto set_c, int k0) {
-    constexpr int set = decltype(set_c)::value;
-#pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int q = tid + i * NT, row = q >> 3, c = q & 7;
-      ra[set][i] = *reinterpret_cast<const frag *>(Ap + size_t(m0 + row) * lda + k0 + c * V);
-    }
-    if constexpr (!KN) {
-#pragma unroll
-      for (int i = 0; i < CB; ++i) {
-        const int q = tid + i * NT, row = q >> 3, c = q & 7;
-        rb[set][i] = *reinterpret_cast<const frag *>(Bp + size_t(n0 + row) * ldb + k0 + c * V);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < QB; ++i) {
-        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          rb[set][4 * i + r] =
-              *reinterpret_cast<const frag *>(Bp + size_t(k0 + 4 * kq + r) * ldb + n0 + nc * V);
-      }
-    }
-  };
-  auto sstore = [&](auto set_c, int buf) {
-    constexpr int set = decltype(set_c)::value;
-    char *sA = smem + buf * S::kStage;
-    char *sB = sA + BM * 128;
-#pragma unroll
-    for (int i = 0; i < CA; ++i) {
-      const int q = tid + i * NT, row = q >> 3, c = q & 7;
-      *reinterpret_cast<frag *>(sA + swz(row, c)) = ra[set][i];
-    }
-    if constexpr (!KN) {
-#pragma unroll
-      for (int i = 0; i < CB; ++i) {
-        const int q = tid + i * NT, row = q >> 3, c = q & 7;
-        *reinterpret_cast<frag *>(sB + swz(row, c)) = rb[set][i];
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < QB; ++i) {
-        const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
-        const int byte = 4 * kq * int(sizeof(T));          // offset of k = 4 kq in the row
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const int n = nc * V + j;
-          quad_t v;
-          v[0] = rb[set][4 * i + 0][j];
-          v[1] = rb[set][4 * i + 1][j];
-          v[2] = rb[set][4 * i + 2][j];
-          v[3] = rb[set][4 * i + 3][j];
-          *reinterpret_cast<quad_t *>(sB + swz(n, byte >> 4) + (byte & 15)) = v;
-        }
-      }
-    }
-  };
 
   // Direct global -> LDS loads (global_load_lds_dwordx4) of the K-major
   // operands: one wave instruction fills 8 consecutive LDS rows (1 KB) at the
@@ -362,44 +298,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     }
   };
 
-  using S0 = std::integral_constant<int, 0>;
-  using S1 = std::integral_constant<int, DEPTH - 1>;
-  // K is a multiple of 128 (padding), BK divides 64, so the slab count is even
+  // K is a multiple of 128 (padding) and BK divides it. One LDS stage is
+  // multiplied while the other is filled by direct loads (and the transposed
+  // update operand) for the next slab.
   const int nk = K / BK;
-  if constexpr (DEPTH == 2) {
-    gload(S0{}, 0);
-    gload(S1{}, BK);
-    sstore(S0{}, 0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-      // LDS stage 0 holds slab kt, set 1 slab kt + 1, set 0 is free
-      if (kt + 2 < nk) gload(S0{}, (kt + 2) * BK);
-      compute(0);
-      sstore(S1{}, 1);
-      __syncthreads();
-      // LDS stage 1 holds slab kt + 1, set 0 slab kt + 2, set 1 is free
-      if (kt + 3 < nk) gload(S1{}, (kt + 3) * BK);
-      compute(1);
-      if (kt + 2 < nk) sstore(S0{}, 0);
-      __syncthreads();
+  dload(0, 0);
+  kload(0);
+  kstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int nb = (kt + 1) & 1;
+    if (kt + 1 < nk) {
+      dload((kt + 1) * BK, nb);
+      kload((kt + 1) * BK);
     }
-  } else {
-    // one LDS stage in use, the other being filled by direct loads (and the
-    // transposed update operand) for the next slab
-    dload(0, 0);
-    kload(0);
-    kstore(0);
+    compute(kt & 1);
+    if (kt + 1 < nk) kstore(nb);
     __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int nb = (kt + 1) & 1;
-      if (kt + 1 < nk) {
-        dload((kt + 1) * BK, nb);
-        kload((kt + 1) * BK);
-      }
-      compute(kt & 1);
-      if (kt + 1 < nk) kstore(nb);
-      __syncthreads();
-    }
   }
 
   // ------------------------------------------------------------ epilogue

@@ -20,7 +20,6 @@
 //              caller's buffer (App. E.3)
 #include <hip/hip_runtime.h>
 
-#include <cstdlib>
 #include <stdexcept>
 #include <string>
 #include <type_traits>
@@ -333,21 +332,21 @@ void check(hipError_t e, const char *what) {
   if (e != hipSuccess) throw HipError(std::string(what) + ": " + hipGetErrorString(e));
 }
 
-template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN, int DEPTH>
+template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
 void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
   switch (op) {
     case Op::Gram:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
     case Op::Poly:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
     case Op::Update:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
     default:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN, DEPTH>), grid, block, 0, s, a);
+      hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
   }
 }
@@ -398,13 +397,9 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         if (l.cfg == kCfg256)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 2, 1>(l.op, grid, a, s);
-        else if (l.cfg == kCfg256w8)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4, 1>(l.op, grid, a, s);
-        else if (std::getenv("SLORR_D128") && std::string(std::getenv("SLORR_D128")) == "2")
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2, 2>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s);
         else
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2, 1>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s);
         break;
       }
       case Op::Finalize:

@@ -4,9 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
-#include <cstdlib>
 #include <map>
-#include <string>
 #include <stdexcept>
 #include <utility>
 
@@ -17,6 +15,7 @@ namespace {
 constexpr int64_t kMaxShort = 16384;
 constexpr int64_t kMaxLong = 1 << 20;
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+constexpr int64_t kMinBigTiles = 2 * 256;   // two 256-tiles per CU (256 CUs)
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
@@ -78,19 +77,22 @@ void build_plan(Plan &p) {
   std::vector<int> order;                 // non-empty matrices
   for (int i = 0; i < p.n; ++i)
     if (!p.mats[i].empty) order.push_back(i);
-  // Tile class per matrix: the 256 x 256 block tile halves the operand
-  // traffic per flop of the 128 x 128 one and needs 256-aligned padded dims.
+  // Tile class of the P x Q products: the 256 x 256 block tile halves the
+  // operand traffic per flop of the 128 x 128 one but needs 256-aligned padded
+  // dims, and gives 4x fewer blocks: it is used only when the set's 256-tiles
+  // still fill the chip twice over (kMinBigTiles). The symmetric P x P
+  // products keep the 128 tile (half of their tiles are mirrored away).
+  int64_t big_tiles = 0;
+  for (int i : order) {
+    const MatDesc &d = p.mats[i];
+    if (d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0)
+      big_tiles += int64_t(d.Pp / kBigTile) * (d.Qp / kBigTile);
+  }
+  const bool use_big = big_tiles >= kMinBigTiles;
   auto upd_cfg = [&](const MatDesc &d) {
-    const char *e = std::getenv("SLORR_UPD_TILE");
-    const std::string v = e ? e : "256w8";
-    if (v == "128" || !(d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0)) return kCfg128;
-    return v == "256w8" ? kCfg256w8 : kCfg256;
+    return (use_big && d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0) ? kCfg256 : kCfg128;
   };
-  auto pp_cfg = [&](const MatDesc &d) {
-    const char *e = std::getenv("SLORR_GRAM_TILE");
-    const bool big = e && std::string(e) == "256";
-    return (big && d.Pp % kBigTile == 0) ? kCfg256 : kCfg128;
-  };
+  auto pp_cfg = [](const MatDesc &) { return kCfg128; };
   auto tsize = [](int cfg) { return cfg == kCfg128 ? kTile : kBigTile; };
   p.tiles.clear();
 
@@ -148,7 +150,7 @@ void build_plan(Plan &p) {
   };
   // Gram and Poly outputs are symmetric: upper-triangle tiles only (the
   // kernel also stores the transpose of off-diagonal tiles)
-  for (int cfg = 0; cfg < 3; ++cfg) {
+  for (int cfg = 0; cfg < kNumCfg; ++cfg) {
     std::vector<Job> jobs;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
@@ -163,7 +165,7 @@ void build_plan(Plan &p) {
   }
   // Update tiles; each owns one trace-partial slot, contiguous per matrix
   int32_t slot = 0;
-  for (int cfg = 0; cfg < 3; ++cfg) {
+  for (int cfg = 0; cfg < kNumCfg; ++cfg) {
     std::vector<Job> jobs;
     for (int i : order) {
       MatDesc &d = p.mats[i];
@@ -255,21 +257,21 @@ void build_plan(Plan &p) {
     const int32_t wx = t & 1;
     const bool quintic = c != 0.0;
     // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
-    for (int cfg = 2; cfg >= 0; --cfg)
+    for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
       gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, 0, float(sa / (double(sx) * sx)), 0.0f, 0.0f);
     const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
     if (quintic) {
       // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
       // the step X' = a X + (b A + c A A) X becomes X' = B X
-      for (int cfg = 2; cfg >= 0; --cfg)
+      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
         gemm(Op::Poly, p.pp[cfg], cfg, wx, 0, 0, float(double(sb) * c / (double(sa) * sa)),
              float(double(sb) * b / sa), float(double(sb) * a));
       // X'_s = (B_s X_s) / s_b
-      for (int cfg = 2; cfg >= 0; --cfg)
+      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
         gemm(op, p.pq[cfg], cfg, wx, 0, 1, float(1.0 / sb), 0.0f, 0.0f);
     } else {
       // cubic step: X'_s = a X_s + b (A_s X_s) / s_a
-      for (int cfg = 2; cfg >= 0; --cfg)
+      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
         gemm(op, p.pq[cfg], cfg, wx, 1, 0, float(b / sa), float(a), 0.0f);
     }
   }

@@ -30,8 +30,8 @@ enum class Op : int {
 // GEMM block-tile configurations (kernel template instances).
 enum GemmCfg : int32_t {
   kCfg128 = 0,   // 128 x 128 block tile, 4 waves of 64 x 64
-  kCfg256 = 1,   // 256 x 256 block tile, 4 waves of 128 x 128
-  kCfg256w8 = 2  // 256 x 256 block tile, 8 waves of 128 x 64
+  kCfg256 = 1,   // 256 x 256 block tile, 8 waves of 128 x 64
+  kNumCfg = 2
 };
 
 struct Launch {
@@ -64,8 +64,8 @@ struct Plan {
   int32_t groups = 0;
   std::vector<MatDesc> mats;
   std::vector<Tile> tiles;             // all tile lists, concatenated
-  TileRange pp[3];                     // P x P outputs (gram, poly), per GemmCfg
-  TileRange pq[3];                     // P x Q outputs (update, last), per GemmCfg
+  TileRange pp[kNumCfg];                     // P x P outputs (gram, poly), per GemmCfg
+  TileRange pq[kNumCfg];                     // P x Q outputs (update, last), per GemmCfg
   TileRange prep;                      // prep tiles over Pp x Qp
   int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
