@@ -40,6 +40,18 @@ def _alg_flops_per_launch(shapes, op):
     return tot
 
 
+def _alg_bytes_per_launch(shapes, dtype, op):
+    """Bytes the memory-bound kernels must move: sumsq reads W (a2); prep reads W
+    and writes X_0 (a3); grad reads W and P and writes the fp32 gradient (a7)."""
+    wb = 2 if dtype == "bf16" else 4          # weight element
+    xb = 2 if dtype == "bf16" else 4          # iterate element (fp16 / fp32)
+    tot = 0
+    for m, n in shapes:
+        e = m * n
+        tot += {"sumsq": wb * e, "prep": (wb + xb) * e, "grad": (wb + xb + 4) * e}[op]
+    return float(tot)
+
+
 def _kernels_hash():
     """Hash of the library's sources (kernels and the plan that orders their tiles)."""
     csrc = os.path.join(ROOT, "paper_2607_08754_amd", "csrc")
@@ -66,18 +78,14 @@ def _traffic(config, op):
     return float(entry) if entry is not None else None
 
 
-def cpu_baseline(cfg, arrs, gpu_vals, gpu_grads, seconds):
-    """The oracle, as it stands, on whole blocks of the set until `seconds`
-    of CPU work; also compares the sampled matrices with the timed GPU output."""
+def _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
+    """Whole blocks of the set through the oracle until `seconds` have passed;
+    returns (blocks done, blocks in the set, seconds, worst value / gradient
+    error of the GPU output on the sampled matrices)."""
     import numpy as np
     from oracle.pe_schedule import pe_schedule
     from oracle.slorr import fwd_bwd
     from workloads import widen
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
-    except Exception:
-        cores = os.cpu_count() or 1
     table = pe_schedule(cfg.iters)
     per_block = 4 if cfg.name.startswith("vit") else 1
     nblocks = cfg.n // per_block
@@ -86,18 +94,31 @@ def cpu_baseline(cfg, arrs, gpu_vals, gpu_grads, seconds):
     while done < nblocks and (time.perf_counter() - t0) < seconds:
         for i in range(done * per_block, (done + 1) * per_block):
             W = widen(arrs[i], cfg.dtype)
-            r = fwd_bwd(W, "hoyer", table)
+            r = fwd_bwd(W, kind, table)
             worst_v = max(worst_v, abs(gpu_vals[i] - r.value) / abs(r.value))
-            s1 = 2.0 * r.n_hat / r.f_eps ** 2
+            s1 = 2.0 * r.n_hat / r.f_eps ** 2 if kind == "hoyer" else 1.0
             den = max(np.linalg.norm(r.grad), np.linalg.norm(s1 * r.polar))
             worst_g = max(worst_g, float(np.linalg.norm(gpu_grads[i] - r.grad) / den))
         done += 1
-    el = time.perf_counter() - t0
-    frac = done * per_block / cfg.n
-    return {"value": frac / el, "unit": "weight-sets/s", "cores": int(cores), "kind": "oracle",
+    return done, nblocks, per_block, time.perf_counter() - t0, worst_v, worst_g
+
+
+def cpu_baseline(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
+    """The oracle, as it stands, on whole blocks of the set: once with every
+    host core the BLAS pool holds, once on a single core (a shorter sample);
+    also compares the sampled matrices with the timed GPU output."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+    cores = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    done, nblocks, per_block, el, wv, wg = _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds)
+    with threadpool_limits(limits=1, user_api="blas"):
+        d1, _, _, el1, _, _ = _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds / 2)
+    return {"value": done * per_block / cfg.n / el, "unit": "weight-sets/s", "cores": int(cores),
+            "kind": "oracle",
             "sample": f"{done} of {nblocks} blocks ({done * per_block} of {cfg.n} matrices), "
                       f"NumPy float64, {el:.1f} s",
-            "parity_on_sample": {"max_value_rel_err": worst_v, "max_grad_rel_err": worst_g}}
+            "one_core": {"value": d1 * per_block / cfg.n / el1, "unit": "weight-sets/s",
+                         "sample": f"{d1} of {nblocks} blocks, {el1:.1f} s"},
+            "parity_on_sample": {"max_value_rel_err": wv, "max_grad_rel_err": wg}}
 
 
 def main():
@@ -182,6 +203,13 @@ def main():
                 "kernel": f"k_gemm<{dominant}>", "alg_flops_per_launch": flops,
                 "avg_launch_ms": op_ms[dominant]["avg_ms"]}
 
+    hbm = {}
+    for op in ("sumsq", "prep", "grad"):
+        if op in op_ms:
+            b = _alg_bytes_per_launch(cfg.shapes, cfg.dtype, op)
+            hbm[op] = {"alg_bytes": b, "avg_ms": op_ms[op]["avg_ms"],
+                       "GB/s": round(b / (op_ms[op]["avg_ms"] * 1e-3) / 1e9, 1)}
+
     value = 1000.0 / ms
     chain_ms = sum(op_ms[o]["ms_per_step"] for o in op_ms if o in GEMM_OPS)
     out = {
@@ -197,10 +225,11 @@ def main():
         "paper_tflops_effective": round(cfg.flops() / (ms * 1e-3) / 1e12, 2),
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
+        "hbm_kernels": hbm,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, arrs, gpu_vals, gpu_grads, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(cfg, arrs, args.kind, gpu_vals, gpu_grads, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
