@@ -85,6 +85,10 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
 #define SLORR_VALUES_ONLY 0x2u  /* values only: no gradient is written, out_grads may be NULL */
 #define SLORR_NO_GRAPH    0x4u  /* enqueue kernels one by one instead of replaying a hipGraph */
 #define SLORR_AUX         0x8u  /* out_vals also receives n_hat_i and f_i (see below) */
+#define SLORR_DEFER_GRAD  0x10u /* slorr_reg_fwd_bwd computes the values and keeps the last
+                                   iterate and the gradient factors in the workspace; the
+                                   gradient is written later by slorr_reg_grad (autograd
+                                   backward, Listing 1). out_grads may be NULL. */
 
 typedef struct {
   int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */
@@ -95,12 +99,14 @@ typedef struct {
                             plan creation. */
   float eps;             /* added to ||W||_F (Listing 1); >= 0 and finite                    */
   uint32_t flags;        /* SLORR_* flags above                                              */
+  slorr_dtype_t grad_dtype; /* element type of the gradient buffers: F32 (default) or BF16
+                            (round to nearest even; for bf16 models whose .grad is bf16) */
 } slorr_options_t;
 
 typedef struct slorr_plan_s *slorr_plan_t;
 
 /* Fill *opts with the defaults: iters 6, degree 5, ell 1e-3, coeffs NULL,
- * eps 0, flags 0. */
+ * eps 0, flags 0, grad_dtype F32. */
 SLORR_API void slorr_default_options(slorr_options_t *opts);
 
 /* Greedy Polar Express schedule (Sec. 3; App. E.1), host only, no device use.
@@ -137,18 +143,65 @@ SLORR_API slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_p
  *   out_vals  : device float array. Receives L_0..L_{n-1} then sum_i L_i (index
  *               order) at out_vals[n]. With SLORR_AUX, also n_hat_i at
  *               out_vals[n+1+i] and ||W_i||_F at out_vals[2n+1+i]. 4-byte aligned.
- *   out_grads : host array of n device pointers to fp32 rows_i x cols_i row-major
- *               buffers, 16-byte aligned, receiving grad_scale * dL_i/dW_i
- *               (or adding it with SLORR_ACCUMULATE). Must not overlap the
- *               weights or each other. May be NULL with SLORR_VALUES_ONLY.
+ *   out_grads : host array of n device pointers to rows_i x cols_i row-major
+ *               buffers of the plan's grad_dtype, 16-byte aligned, receiving
+ *               grad_scale * dL_i/dW_i (or adding it with SLORR_ACCUMULATE).
+ *               Must not overlap the weights or each other. May be NULL with
+ *               SLORR_VALUES_ONLY or SLORR_DEFER_GRAD.
  *   grad_scale: upstream factor g (e.g. lambda times the upstream gradient).
  *   stream    : hipStream_t to enqueue on (NULL = the null stream).
  * A matrix whose ||W||_F + eps is 0 gets value 0 and gradient 0; NaN or Inf in
- * a matrix propagate to that matrix's outputs and to the sum only. */
+ * a matrix propagate to that matrix's outputs and to the sum only.
+ *
+ * Gradient rounding (both entry points): with s1, s2 the factors of Eq.
+ * SLORR_grads (Hoyer: s1 = 2 n/(f+eps)^2, s2 = 2 n^2/(f+eps)^4; nuclear: s1 = 1,
+ * s2 = 0), each element is t = s1 P - s2 W in fp32, then u = fl(g * t), then
+ * fl(old + u) with SLORR_ACCUMULATE. For BF16 gradients u is rounded to bf16
+ * first and the accumulated sum is rounded again. So a deferred gradient with
+ * scale g, added to a buffer afterwards, is bit-identical to an accumulating
+ * call with grad_scale = g (the autograd and hook integrations of App. E.3). */
 SLORR_API slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const *weights,
                                  const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
-                                 float *out_vals, float *const *out_grads, float grad_scale,
+                                 float *out_vals, void *const *out_grads, float grad_scale,
                                  void *stream);
+
+/* Gradient from the state a preceding slorr_reg_fwd_bwd on this plan left in
+ * the workspace (the last iterate P and the factors s1, s2): the backward half
+ * of a forward run with SLORR_DEFER_GRAD (or any run that wrote gradients).
+ *   n, weights, shapes, kind, iters : as in that call; weights must hold the
+ *               same values (the Hoyer gradient reads W again).
+ *   out_grads : as in slorr_reg_fwd_bwd (grad_dtype, alignment, no overlap),
+ *               written or, with SLORR_ACCUMULATE, added to.
+ *   scales    : device array of n floats or NULL; matrix i gets the upstream
+ *               factor g_i = fl(grad_scale * scales[i]) (grad_scale if NULL).
+ *               Autograd passes the incoming gradient of the value vector here,
+ *               so no host synchronisation is needed.
+ * The state stays valid until the next slorr_reg_fwd_bwd or
+ * slorr_plan_set_workspace on the plan; calling this function before any
+ * state exists (or after a SLORR_VALUES_ONLY run) is SLORR_ERR_INVALID_ARGUMENT.
+ * Stream-ordered: it must be enqueued after the forward call (same stream, or
+ * synchronised). One kernel launch, no graph. */
+SLORR_API slorr_status_t slorr_reg_grad(slorr_plan_t plan, int32_t n, const void *const *weights,
+                                 const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                                 void *const *out_grads, const float *scales, float grad_scale,
+                                 void *stream);
+
+/* Decoupled SLORR update (App. E.2, Alg. 1), applied after the optimizer step:
+ *   W_i <- W_i - s_i G_i,   s_i = fl(step * steps[i])  (step if steps is NULL)
+ * with G_i the pre-update gradient a slorr_reg_fwd_bwd (grad_scale 1) wrote
+ * before the step. Per element fl(w - fl(s_i g)) in fp32, then one rounding
+ * (to nearest even) to the plan's weight dtype.
+ *   weights : host array of n device pointers to the weights, updated in place
+ *             (plan dtype, 16-byte aligned)
+ *   grads   : host array of n device pointers of the plan's grad_dtype; must not
+ *             overlap the weights or each other
+ *   steps   : device array of n floats (e.g. per-group learning rates) or NULL
+ *   step    : scalar factor (e.g. eta * lambda, or lambda with steps = eta)
+ * The plan's kind and iters are not used; the state of slorr_reg_grad is kept.
+ * One kernel launch on `stream`, no graph. */
+SLORR_API slorr_status_t slorr_decoupled_apply(slorr_plan_t plan, int32_t n, void *const *weights,
+                                 const slorr_shape_t *shapes, const void *const *grads,
+                                 const float *steps, float step, void *stream);
 
 /* Kernel kinds of the launch schedule, as reported by slorr_reg_fwd_bwd_profiled. */
 typedef enum {
@@ -172,7 +225,7 @@ typedef enum {
 SLORR_API slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
                                  const void *const *weights, const slorr_shape_t *shapes,
                                  slorr_kind_t kind, int32_t iters, float *out_vals,
-                                 float *const *out_grads, float grad_scale, void *stream,
+                                 void *const *out_grads, float grad_scale, void *stream,
                                  float *launch_ms, int32_t *launch_op);
 
 /* Release the plan (and its captured graph). Does not free the workspace.

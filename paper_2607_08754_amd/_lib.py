@@ -26,11 +26,13 @@ ACCUMULATE = 0x1
 VALUES_ONLY = 0x2
 NO_GRAPH = 0x4
 AUX = 0x8
+DEFER_GRAD = 0x10
 
 OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad")
 
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
-            "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_fwd_bwd_profiled",
+            "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",
+            "slorr_reg_fwd_bwd_profiled",
             "slorr_plan_destroy", "slorr_plan_get_info", "slorr_status_string", "slorr_last_error")
 
 
@@ -41,7 +43,7 @@ class Shape(ctypes.Structure):
 class Options(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("degree", ctypes.c_int32), ("ell", ctypes.c_double),
                 ("coeffs", ctypes.POINTER(ctypes.c_double)), ("eps", ctypes.c_float),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("grad_dtype", ctypes.c_int)]
 
 
 class PlanInfo(ctypes.Structure):
@@ -85,6 +87,12 @@ def lib() -> ctypes.CDLL:
         L.slorr_reg_fwd_bwd.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape), ctypes.c_int,
                                         i32, vp, ctypes.POINTER(vp), ctypes.c_float, vp]
         L.slorr_reg_fwd_bwd.restype = ctypes.c_int
+        L.slorr_reg_grad.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape), ctypes.c_int,
+                                     i32, ctypes.POINTER(vp), vp, ctypes.c_float, vp]
+        L.slorr_reg_grad.restype = ctypes.c_int
+        L.slorr_decoupled_apply.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape),
+                                            ctypes.POINTER(vp), vp, ctypes.c_float, vp]
+        L.slorr_decoupled_apply.restype = ctypes.c_int
         L.slorr_reg_fwd_bwd_profiled.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape),
                                                  ctypes.c_int, i32, vp, ctypes.POINTER(vp), ctypes.c_float, vp,
                                                  ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]

@@ -78,89 +78,113 @@ void release_runtime(slorr::Plan &p) {
   p.dyn_valid = false;
 }
 
-// Validates a call against the plan and uploads the per-call pointer table
-// (only when it changed). Returns the plan; nothing is enqueued on failure
-// except when the table upload itself fails.
+// Checks the arguments every entry point shares against the plan.
+slorr::Plan &check_call(slorr_plan_t plan, int32_t n, const void *const *weights,
+                        const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters) {
+  if (!plan) throw std::invalid_argument("plan is NULL");
+  slorr::Plan &p = plan->p;
+  if (n != p.n) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "n differs from the plan"};
+  if (kind != p.kind) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "kind differs from the plan"};
+  if (iters != p.iters) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "iters differs from the plan"};
+  if (n > 0 && !shapes) throw std::invalid_argument("shapes is NULL");
+  for (int i = 0; i < n; ++i)
+    if (shapes[i].rows != p.shapes[i].rows || shapes[i].cols != p.shapes[i].cols)
+      throw ApiError{SLORR_ERR_PLAN_MISMATCH, "shape of matrix " + std::to_string(i) + " differs from the plan"};
+  if (n > 0 && !weights) throw std::invalid_argument("weights is NULL");
+  return p;
+}
+
+// Pointer checks of weights and (if want_grad) gradient buffers, and that no
+// gradient range overlaps a weight range or another gradient range.
+void check_buffers(const slorr::Plan &p, const void *const *weights, void *const *out_grads,
+                   bool want_grad) {
+  const int n = p.n;
+  if (want_grad && n > 0 && !out_grads) throw std::invalid_argument("out_grads is NULL");
+  std::vector<std::pair<uintptr_t, std::pair<uintptr_t, int>>> spans;  // begin, (end, is_grad)
+  for (int i = 0; i < n; ++i) {
+    const slorr::MatDesc &d = p.mats[i];
+    if (d.empty) continue;
+    const size_t elems = size_t(d.rows) * d.cols;
+    if (!weights[i]) throw std::invalid_argument("weights[" + std::to_string(i) + "] is NULL");
+    if (!aligned(weights[i], 16)) throw std::invalid_argument("weights[" + std::to_string(i) + "] must be 16-byte aligned");
+    const uintptr_t wb = reinterpret_cast<uintptr_t>(weights[i]);
+    spans.push_back({wb, {wb + elems * p.elem_bytes(), 0}});
+    if (want_grad) {
+      if (!out_grads[i]) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] is NULL");
+      if (!aligned(out_grads[i], 16)) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] must be 16-byte aligned");
+      const uintptr_t gb = reinterpret_cast<uintptr_t>(out_grads[i]);
+      spans.push_back({gb, {gb + elems * p.grad_bytes(), 1}});
+    }
+  }
+  std::sort(spans.begin(), spans.end());
+  uintptr_t reach_all = 0, reach_grad = 0;   // furthest end of earlier spans / grad spans
+  for (const auto &s : spans) {
+    const bool is_grad = s.second.second != 0;
+    if (s.first < reach_grad || (is_grad && s.first < reach_all))
+      throw std::invalid_argument("out_grads overlap the weights or each other");
+    reach_all = std::max(reach_all, s.second.first);
+    if (is_grad) reach_grad = std::max(reach_grad, s.second.first);
+  }
+}
+
+void check_device(const slorr::Plan &p) {
+  if (!p.ws) throw ApiError{SLORR_ERR_WORKSPACE, "no workspace attached to the plan"};
+  int dev = -1;
+  hip_check(hipGetDevice(&dev), "hipGetDevice");
+  if (dev != p.device) throw std::invalid_argument("current device differs from the workspace's device");
+}
+
+// Uploads the per-call pointer table and call parameters on stream s, only
+// when they differ from what the workspace holds. The pinned staging buffer
+// is reused only after its previous copy has completed.
+void upload_call(slorr::Plan &p, const void *const *weights, void *const *out_grads, bool want_grad,
+                 const slorr::CallParams &call, hipStream_t s) {
+  const int n = p.n;
+  std::vector<slorr::DynDesc> dyn(n);
+  for (int i = 0; i < n; ++i) {
+    dyn[i].w = p.mats[i].empty ? nullptr : weights[i];
+    dyn[i].g = (want_grad && !p.mats[i].empty) ? out_grads[i] : nullptr;
+  }
+  const bool same = p.dyn_valid && p.call_cache.out_vals == call.out_vals &&
+                    p.call_cache.gscale == call.gscale &&
+                    std::memcmp(&p.call_cache.grad_scale, &call.grad_scale, sizeof(float)) == 0 &&
+                    std::memcmp(p.dyn_cache.data(), dyn.data(), n * sizeof(slorr::DynDesc)) == 0;
+  if (same) return;
+  const int k = p.staging_next;
+  p.staging_next ^= 1;
+  hipEvent_t ev = static_cast<hipEvent_t>(p.staging_event[k]);
+  hip_check(hipEventSynchronize(ev), "hipEventSynchronize");
+  char *st = static_cast<char *>(p.staging[k]);
+  std::memset(st, 0, p.dyn_bytes());
+  if (n) std::memcpy(st, dyn.data(), n * sizeof(slorr::DynDesc));
+  std::memcpy(st + (p.off_call - p.off_dyn), &call, sizeof(call));
+  hip_check(hipMemcpyAsync(static_cast<char *>(p.ws) + p.off_dyn, st, p.dyn_bytes(),
+                           hipMemcpyHostToDevice, s),
+            "hipMemcpyAsync pointer table");
+  hip_check(hipEventRecord(ev, s), "hipEventRecord");
+  p.dyn_cache = dyn;
+  p.call_cache = call;
+  p.dyn_valid = true;
+}
+
+// Validates a forward call against the plan and uploads its tables. Returns
+// the plan; nothing is enqueued on failure except when the upload itself fails.
 slorr::Plan &prepare_call(slorr_plan_t plan, int32_t n, const void *const *weights,
                           const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
-                          float *out_vals, float *const *out_grads, float grad_scale,
+                          float *out_vals, void *const *out_grads, float grad_scale,
                           hipStream_t s) {
-    if (!plan) throw std::invalid_argument("plan is NULL");
-    slorr::Plan &p = plan->p;
-    if (n != p.n) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "n differs from the plan"};
-    if (kind != p.kind) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "kind differs from the plan"};
-    if (iters != p.iters) throw ApiError{SLORR_ERR_PLAN_MISMATCH, "iters differs from the plan"};
-    if (n > 0 && !shapes) throw std::invalid_argument("shapes is NULL");
-    for (int i = 0; i < n; ++i)
-      if (shapes[i].rows != p.shapes[i].rows || shapes[i].cols != p.shapes[i].cols)
-        throw ApiError{SLORR_ERR_PLAN_MISMATCH, "shape of matrix " + std::to_string(i) + " differs from the plan"};
-    if (!out_vals) throw std::invalid_argument("out_vals is NULL");
-    if (!aligned(out_vals, 4)) throw std::invalid_argument("out_vals must be 4-byte aligned");
-    const bool want_grad = !(p.flags & SLORR_VALUES_ONLY);
-    if (n > 0 && !weights) throw std::invalid_argument("weights is NULL");
-    if (want_grad && n > 0 && !out_grads) throw std::invalid_argument("out_grads is NULL");
-    // pointer checks and overlap of written ranges
-    std::vector<std::pair<uintptr_t, std::pair<uintptr_t, int>>> spans;  // begin, (end, is_grad)
-    for (int i = 0; i < n; ++i) {
-      const slorr::MatDesc &d = p.mats[i];
-      if (d.empty) continue;
-      const size_t elems = size_t(d.rows) * d.cols;
-      if (!weights[i]) throw std::invalid_argument("weights[" + std::to_string(i) + "] is NULL");
-      if (!aligned(weights[i], 16)) throw std::invalid_argument("weights[" + std::to_string(i) + "] must be 16-byte aligned");
-      const uintptr_t wb = reinterpret_cast<uintptr_t>(weights[i]);
-      spans.push_back({wb, {wb + elems * p.elem_bytes(), 0}});
-      if (want_grad) {
-        if (!out_grads[i]) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] is NULL");
-        if (!aligned(out_grads[i], 16)) throw std::invalid_argument("out_grads[" + std::to_string(i) + "] must be 16-byte aligned");
-        const uintptr_t gb = reinterpret_cast<uintptr_t>(out_grads[i]);
-        spans.push_back({gb, {gb + elems * sizeof(float), 1}});
-      }
-    }
-    std::sort(spans.begin(), spans.end());
-    uintptr_t reach_all = 0, reach_grad = 0;   // furthest end of earlier spans / grad spans
-    for (const auto &s : spans) {
-      const bool is_grad = s.second.second != 0;
-      if (s.first < reach_grad || (is_grad && s.first < reach_all))
-        throw std::invalid_argument("out_grads overlap the weights or each other");
-      reach_all = std::max(reach_all, s.second.first);
-      if (is_grad) reach_grad = std::max(reach_grad, s.second.first);
-    }
-    if (!p.ws) throw ApiError{SLORR_ERR_WORKSPACE, "no workspace attached to the plan"};
-    int dev = -1;
-    hip_check(hipGetDevice(&dev), "hipGetDevice");
-    if (dev != p.device) throw std::invalid_argument("current device differs from the workspace's device");
-
-    // per-call pointer table: upload only when it changed
-    std::vector<slorr::DynDesc> dyn(n);
-    for (int i = 0; i < n; ++i) {
-      dyn[i].w = p.mats[i].empty ? nullptr : weights[i];
-      dyn[i].g = (want_grad && !p.mats[i].empty) ? out_grads[i] : nullptr;
-    }
-    slorr::CallParams call{};
-    call.out_vals = out_vals;
-    call.grad_scale = grad_scale;
-    const bool same = p.dyn_valid && p.call_cache.out_vals == call.out_vals &&
-                      p.call_cache.grad_scale == call.grad_scale &&
-                      std::memcmp(p.dyn_cache.data(), dyn.data(), n * sizeof(slorr::DynDesc)) == 0;
-    if (!same) {
-      const int k = p.staging_next;
-      p.staging_next ^= 1;
-      hipEvent_t ev = static_cast<hipEvent_t>(p.staging_event[k]);
-      hip_check(hipEventSynchronize(ev), "hipEventSynchronize");
-      char *st = static_cast<char *>(p.staging[k]);
-      std::memset(st, 0, p.dyn_bytes());
-      if (n) std::memcpy(st, dyn.data(), n * sizeof(slorr::DynDesc));
-      std::memcpy(st + (p.off_call - p.off_dyn), &call, sizeof(call));
-      hip_check(hipMemcpyAsync(static_cast<char *>(p.ws) + p.off_dyn, st, p.dyn_bytes(),
-                               hipMemcpyHostToDevice, s),
-                "hipMemcpyAsync pointer table");
-      hip_check(hipEventRecord(ev, s), "hipEventRecord");
-      p.dyn_cache = dyn;
-      p.call_cache = call;
-      p.dyn_valid = true;
-    }
-
-    return p;
+  slorr::Plan &p = check_call(plan, n, weights, shapes, kind, iters);
+  if (!out_vals) throw std::invalid_argument("out_vals is NULL");
+  if (!aligned(out_vals, 4)) throw std::invalid_argument("out_vals must be 4-byte aligned");
+  const bool want_grad = !(p.flags & (SLORR_VALUES_ONLY | SLORR_DEFER_GRAD));
+  check_buffers(p, weights, out_grads, want_grad);
+  check_device(p);
+  slorr::CallParams call{};
+  call.out_vals = out_vals;
+  call.gscale = nullptr;
+  call.grad_scale = grad_scale;
+  upload_call(p, weights, out_grads, want_grad, call, s);
+  return p;
 }
 
 }  // namespace
@@ -175,6 +199,7 @@ void slorr_default_options(slorr_options_t *o) {
   o->coeffs = nullptr;
   o->eps = 0.0f;
   o->flags = 0;
+  o->grad_dtype = SLORR_F32;
 }
 
 slorr_status_t slorr_pe_coefficients(double ell, int32_t degree, int32_t iters, double *out) {
@@ -211,6 +236,7 @@ slorr_status_t slorr_plan_create(slorr_plan_t *plan, int32_t n, const slorr_shap
       p.ell = o.ell == 0.0 ? 1e-3 : o.ell;
       p.eps = o.eps;
       p.flags = o.flags;
+      p.grad_dtype = o.grad_dtype;
       p.shapes.assign(shapes, shapes + n);
       if (o.coeffs) {
         if (p.iters < 1 || p.iters > 1000) throw std::invalid_argument("iters must be in [1, 1000]");
@@ -260,6 +286,7 @@ slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t
                                               " bytes, got " + std::to_string(bytes)};
     release_runtime(p);
     p.ws = nullptr;
+    p.state_ready = false;
     int dev = -1;
     hip_check(hipGetDevice(&dev), "hipGetDevice");
     // static tables, one synchronous copy
@@ -286,14 +313,16 @@ slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t
 
 slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const *weights,
                                  const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
-                                 float *out_vals, float *const *out_grads, float grad_scale,
+                                 float *out_vals, void *const *out_grads, float grad_scale,
                                  void *stream) {
   return guarded([&]() -> slorr_status_t {
     hipStream_t s = static_cast<hipStream_t>(stream);
     slorr::Plan &p = prepare_call(plan, n, weights, shapes, kind, iters, out_vals, out_grads,
                                   grad_scale, s);
+    p.state_ready = false;
     if (p.flags & SLORR_NO_GRAPH) {
       slorr::enqueue(p, s);
+      p.state_ready = !(p.flags & SLORR_VALUES_ONLY);
       return SLORR_OK;
     }
     if (!p.graph_exec) {
@@ -317,6 +346,50 @@ slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const
       p.graph_exec = ge;
     }
     hip_check(hipGraphLaunch(static_cast<hipGraphExec_t>(p.graph_exec), s), "hipGraphLaunch");
+    p.state_ready = !(p.flags & SLORR_VALUES_ONLY);
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_reg_grad(slorr_plan_t plan, int32_t n, const void *const *weights,
+                              const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                              void *const *out_grads, const float *scales, float grad_scale,
+                              void *stream) {
+  return guarded([&]() -> slorr_status_t {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    slorr::Plan &p = check_call(plan, n, weights, shapes, kind, iters);
+    if (p.flags & SLORR_VALUES_ONLY)
+      throw std::invalid_argument("the plan computes values only (SLORR_VALUES_ONLY)");
+    if (!p.state_ready) throw std::invalid_argument("no forward state: run slorr_reg_fwd_bwd on this plan first");
+    if (scales && !aligned(scales, 4)) throw std::invalid_argument("scales must be 4-byte aligned");
+    check_buffers(p, weights, out_grads, true);
+    check_device(p);
+    slorr::CallParams call = p.call_cache;     // keeps out_vals of the forward call
+    call.gscale = scales;
+    call.grad_scale = grad_scale;
+    upload_call(p, weights, out_grads, true, call, s);
+    slorr::enqueue_grad(p, s);
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_decoupled_apply(slorr_plan_t plan, int32_t n, void *const *weights,
+                                     const slorr_shape_t *shapes, const void *const *grads,
+                                     const float *steps, float step, void *stream) {
+  return guarded([&]() -> slorr_status_t {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!plan) throw std::invalid_argument("plan is NULL");
+    const void *const *w = reinterpret_cast<const void *const *>(weights);
+    void *const *g = const_cast<void *const *>(grads);
+    slorr::Plan &p = check_call(plan, n, w, shapes, plan->p.kind, plan->p.iters);
+    if (steps && !aligned(steps, 4)) throw std::invalid_argument("steps must be 4-byte aligned");
+    check_buffers(p, w, g, true);
+    check_device(p);
+    slorr::CallParams call = p.call_cache;
+    call.gscale = steps;
+    call.grad_scale = step;
+    upload_call(p, w, g, true, call, s);
+    slorr::enqueue_apply(p, s);
     return SLORR_OK;
   });
 }
@@ -324,7 +397,7 @@ slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const void *const
 slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
                                           const void *const *weights, const slorr_shape_t *shapes,
                                           slorr_kind_t kind, int32_t iters, float *out_vals,
-                                          float *const *out_grads, float grad_scale, void *stream,
+                                          void *const *out_grads, float grad_scale, void *stream,
                                           float *launch_ms, int32_t *launch_op) {
   return guarded([&]() -> slorr_status_t {
     if (!launch_ms) throw std::invalid_argument("launch_ms is NULL");
@@ -341,7 +414,9 @@ slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
       }
     } guard{ev};
     for (auto &e : ev) hip_check(hipEventCreate(&e), "hipEventCreate");
+    p.state_ready = false;
     slorr::enqueue(p, s, ev.data());
+    p.state_ready = !(p.flags & SLORR_VALUES_ONLY);
     hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
     for (size_t i = 0; i < nl; ++i) {
       float ms = 0.0f;

@@ -18,6 +18,7 @@
 //   k_grad     grad = g (s1 P - s2 W)  (Hoyer) or g P (nuclear) from the last
 //              iterate, in W's orientation, optionally accumulated into the
 //              caller's buffer (App. E.3)
+//   k_apply    W <- W - s G_pre, the decoupled update (App. E.2, Alg. 1)
 #include <hip/hip_runtime.h>
 
 #include <stdexcept>
@@ -42,9 +43,20 @@ __device__ __forceinline__ float to_f(float v) { return v; }
 __device__ __forceinline__ float to_f(bf16_t v) { return __uint_as_float(uint32_t(v) << 16); }
 __device__ __forceinline__ float to_f(_Float16 v) { return float(v); }
 
+// fp32 -> bf16 with round to nearest, ties to even (a NaN stays a quiet NaN):
+// add half an ulp of the bf16 result, minus one when the kept part is even,
+// then truncate.
+__device__ __forceinline__ bf16_t f32_to_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return bf16_t(u >> 16);
+}
+
 template <typename T> __device__ __forceinline__ T from_f(float v);
 template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
 template <> __device__ __forceinline__ _Float16 from_f<_Float16>(float v) { return _Float16(v); }
+template <> __device__ __forceinline__ bf16_t from_f<bf16_t>(float v) { return f32_to_bf16(v); }
 
 // Sum over the NT threads of a block: butterfly within each wave, then the
 // per-wave sums in wave order. Fixed order, so bitwise reproducible. The
@@ -101,11 +113,17 @@ __device__ __forceinline__ void get8(const T *p, int n, float (&v)[8]) {
 template <typename T>
 __device__ __forceinline__ void put8(T *p, int n, const float (&v)[8]) {
   if (n >= 8 && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
-    if constexpr (sizeof(T) == 2) {
+    if constexpr (std::is_same<T, _Float16>::value) {
       half8 h;
 #pragma unroll
       for (int j = 0; j < 8; ++j) h[j] = _Float16(v[j]);
       *reinterpret_cast<half8 *>(p) = h;
+    } else if constexpr (sizeof(T) == 2) {
+      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+      u16x8 h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) h[j] = from_f<T>(v[j]);
+      *reinterpret_cast<u16x8 *>(p) = h;
     } else {
       float4v a, b;
 #pragma unroll
@@ -229,7 +247,6 @@ __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict
                                                        const CallParams *__restrict__ call,
                                                        int n, int kind, int aux) {
   float *out = call->out_vals;
-  const double g = double(call->grad_scale);
   const int lane = threadIdx.x & 63;
   for (int i = threadIdx.x >> 6; i < n; i += kThreads / 64) {
     const MatDesc d = mats[i];
@@ -238,22 +255,22 @@ __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict
     nh = wave_sum(nh);
     if (lane != 0) continue;
     const double fe = d.empty ? 0.0 : sc[i].feps;
-    double L = 0.0, c1 = 0.0, c2 = 0.0;
+    double L = 0.0, s1 = 0.0, s2 = 0.0;
     if (d.empty || fe == 0.0) {
       nh = 0.0;
     } else if (kind == SLORR_HOYER) {
       const double r = nh / fe;           // n / (f + eps)
       L = r * r;
-      c1 = g * 2.0 * nh / (fe * fe);      // g 2 r / (f + eps)
-      c2 = g * 2.0 * nh * nh / (fe * fe * fe * fe);  // g 2 r n / (f + eps)^3
+      s1 = 2.0 * nh / (fe * fe);          // 2 r / (f + eps)
+      s2 = 2.0 * nh * nh / (fe * fe * fe * fe);  // 2 r n / (f + eps)^3
     } else {
       L = nh;
-      c1 = g;
+      s1 = 1.0;
     }
     sc[i].nhat = nh;
     sc[i].value = L;
-    sc[i].c1 = c1;
-    sc[i].c2 = c2;
+    sc[i].s1 = s1;
+    sc[i].s2 = s2;
     out[i] = float(L);
     if (aux) {
       out[n + 1 + i] = float(nh);
@@ -272,17 +289,21 @@ __global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict
 // ---------------------------------------------------------------- gradient
 
 // Gradient in W's own orientation from the last iterate X_T (canonical,
-// zero-padded, scale s_x): grad = c1 X_T / s_x - c2 W (+ grad). One block per
-// 64 x 64 canonical tile: X_T rows are read 8 at a time, staged in LDS (fp32)
-// and read back along W's rows (transposed for tall W), so that W and grad
-// are accessed 8 consecutive elements at a time.
-template <typename Tw, typename Tx>
+// zero-padded, scale s_x): t = s1 X_T / s_x - s2 W, u = g t, grad = u or
+// grad + u. One block per 64 x 64 canonical tile: X_T rows are read 8 at a
+// time, staged in LDS (fp32) and read back along W's rows (transposed for tall
+// W), so that W and grad are accessed 8 consecutive elements at a time.
+// Contraction is off: each product and sum is rounded on its own, so the
+// result for a factor g equals fl(g * t) added to the buffer afterwards.
+template <typename Tw, typename Tx, typename Tg>
 __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tiles,
                                                    const MatDesc *__restrict__ mats,
                                                    const DynDesc *__restrict__ dyn,
                                                    const Scalars *__restrict__ sc,
+                                                   const CallParams *__restrict__ call,
                                                    const char *__restrict__ ws, int xsel, float inv_sx,
                                                    int accumulate) {
+#pragma clang fp contract(off)
   __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
   const Tile t = tiles[blockIdx.x];
   const MatDesc d = mats[t.mat];
@@ -290,8 +311,9 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   if (m0 >= d.P || n0 >= d.Q) return;                    // padding only (whole block)
   const Tx *x = reinterpret_cast<const Tx *>(ws + (xsel ? d.x1 : d.x0));
   const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
-  float *g = dyn[t.mat].g;
-  const float c1 = float(sc[t.mat].c1) * inv_sx, c2 = float(sc[t.mat].c2);
+  Tg *g = static_cast<Tg *>(dyn[t.mat].g);
+  const float s1 = float(sc[t.mat].s1) * inv_sx, s2 = float(sc[t.mat].s2);
+  const float gs = call->gscale ? call->grad_scale * call->gscale[t.mat] : call->grad_scale;
   for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
     float v[8];
@@ -312,15 +334,46 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float p = d.tall ? tile[(c + j) * kPrepPitch + r] : tile[r * kPrepPitch + c + j];
-      v[j] = c1 * p - c2 * wv[j];
+      const float tj = s1 * p - s2 * wv[j];
+      v[j] = gs * tj;
+      if constexpr (sizeof(Tg) == 2) v[j] = to_f(from_f<Tg>(v[j]));   // u rounded to bf16
     }
     if (accumulate) {
       float old[8];
       get8(g + o, nv, old);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] += old[j];
+      for (int j = 0; j < 8; ++j) v[j] = old[j] + v[j];
     }
     put8(g + o, nv, v);
+  }
+}
+
+// ------------------------------------------------------------ decoupled
+
+// Decoupled update of the weights (App. E.2, Alg. 1): W <- W - s G_pre with
+// s = the per-matrix step. Per element fl(w - fl(s g)) in fp32 (no
+// contraction), then one rounding to W's type. One block per chunk of the
+// norm kernel's element runs.
+template <typename Tw, typename Tg>
+__global__ __launch_bounds__(kThreads) void k_apply(const Chunk *__restrict__ chunks,
+                                                    const DynDesc *__restrict__ dyn,
+                                                    const CallParams *__restrict__ call) {
+#pragma clang fp contract(off)
+  const Chunk ch = chunks[blockIdx.x];
+  Tw *w = static_cast<Tw *>(const_cast<void *>(dyn[ch.mat].w)) + ch.begin;
+  const Tg *g = static_cast<const Tg *>(dyn[ch.mat].g) + ch.begin;
+  const float st = call->gscale ? call->grad_scale * call->gscale[ch.mat] : call->grad_scale;
+  for (int i = threadIdx.x * 8; i < ch.len; i += kThreads * 8) {
+    const int nv = min(8, ch.len - i);
+    float wv[8], gv[8];
+    get8(w + i, nv, wv);
+    get8(g + i, nv, gv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float u = st * gv[j];
+      wv[j] = wv[j] - u;
+    }
+    put8(w + i, nv, wv);
   }
 }
 
@@ -349,6 +402,24 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s) {
       hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
   }
+}
+
+template <typename Tw, typename Tx>
+void launch_grad(const Plan &p, const Launch &l, hipStream_t s) {
+  const char *ws = static_cast<const char *>(p.ws);
+  const Tile *tiles = reinterpret_cast<const Tile *>(ws + p.off_tiles) + l.tile_first;
+  const MatDesc *mats = reinterpret_cast<const MatDesc *>(ws + p.off_mats);
+  const DynDesc *dyn = reinterpret_cast<const DynDesc *>(ws + p.off_dyn);
+  const Scalars *sc = reinterpret_cast<const Scalars *>(ws + p.off_scal);
+  const CallParams *call = reinterpret_cast<const CallParams *>(ws + p.off_call);
+  const float inv_sx = 1.0f / (sizeof(Tx) == 2 ? kScaleX16 : 1.0f);
+  const int acc = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
+  if (p.grad_dtype == SLORR_BF16)
+    hipLaunchKernelGGL((k_grad<Tw, Tx, bf16_t>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
+                       call, ws, l.which_x, inv_sx, acc);
+  else
+    hipLaunchKernelGGL((k_grad<Tw, Tx, float>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
+                       call, ws, l.which_x, inv_sx, acc);
 }
 
 template <typename Tw, typename Tx>
@@ -407,8 +478,7 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
                            (p.flags & SLORR_AUX) ? 1 : 0);
         break;
       case Op::Grad:
-        hipLaunchKernelGGL((k_grad<Tw, Tx>), grid, block, 0, s, tiles + l.tile_first, mats, dyn, sc, ws,
-                           l.which_x, 1.0f / sx, (p.flags & SLORR_ACCUMULATE) ? 1 : 0);
+        launch_grad<Tw, Tx>(p, l, s);
         break;
     }
     check(hipGetLastError(), "kernel launch");
@@ -423,6 +493,33 @@ void enqueue(const Plan &p, hipStream_t s, hipEvent_t *events) {
     enqueue_typed<bf16_t, _Float16>(p, s, events);
   else
     enqueue_typed<float, float>(p, s, events);
+}
+
+void enqueue_apply(const Plan &p, hipStream_t s) {
+  if (p.chunks.empty()) return;
+  const char *ws = static_cast<const char *>(p.ws);
+  const Chunk *chunks = reinterpret_cast<const Chunk *>(ws + p.off_chunks);
+  const DynDesc *dyn = reinterpret_cast<const DynDesc *>(ws + p.off_dyn);
+  const CallParams *call = reinterpret_cast<const CallParams *>(ws + p.off_call);
+  const dim3 grid(uint32_t(p.chunks.size())), block(kThreads);
+  const bool gb = p.grad_dtype == SLORR_BF16;
+  if (p.dtype == SLORR_BF16) {
+    if (gb) hipLaunchKernelGGL((k_apply<bf16_t, bf16_t>), grid, block, 0, s, chunks, dyn, call);
+    else hipLaunchKernelGGL((k_apply<bf16_t, float>), grid, block, 0, s, chunks, dyn, call);
+  } else {
+    if (gb) hipLaunchKernelGGL((k_apply<float, bf16_t>), grid, block, 0, s, chunks, dyn, call);
+    else hipLaunchKernelGGL((k_apply<float, float>), grid, block, 0, s, chunks, dyn, call);
+  }
+  check(hipGetLastError(), "kernel launch");
+}
+
+void enqueue_grad(const Plan &p, hipStream_t s) {
+  if (!p.grad_launch.grid) return;
+  if (p.dtype == SLORR_BF16)
+    launch_grad<bf16_t, _Float16>(p, p.grad_launch, s);
+  else
+    launch_grad<float, float>(p, p.grad_launch, s);
+  check(hipGetLastError(), "kernel launch");
 }
 
 }  // namespace slorr

@@ -40,11 +40,12 @@ struct MatDesc {
 
 struct DynDesc {               // per call: caller pointers
   const void *w;
-  float *g;
+  void *g;                     // gradient buffer (fp32 or bf16)
 };
 
 struct CallParams {            // per call
   float *out_vals;
+  const float *gscale;         // per-matrix upstream factors (device) or null
   float grad_scale;
   int32_t pad;
 };
@@ -58,7 +59,8 @@ struct Chunk {                 // a contiguous run of a matrix's elements
 };
 
 struct Scalars {               // per matrix, written by the kernels
-  double sumsq, f, feps, nhat, value, c1, c2;
+  double sumsq, f, feps, nhat, value;
+  double s1, s2;               // gradient = g (s1 P - s2 W)
   float inv_feps, pad;
 };
 

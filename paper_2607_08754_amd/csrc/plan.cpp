@@ -32,8 +32,13 @@ void build_plan(Plan &p) {
   if (p.degree != 3 && p.degree != 5) throw std::domain_error("degree must be 3 or 5");
   if (!(p.ell > 0.0 && p.ell < 1.0)) throw std::invalid_argument("ell must be in (0, 1)");
   if (!(p.eps >= 0.0f) || !std::isfinite(p.eps)) throw std::invalid_argument("eps must be finite and >= 0");
-  if (p.flags & ~uint32_t(SLORR_ACCUMULATE | SLORR_VALUES_ONLY | SLORR_NO_GRAPH | SLORR_AUX))
+  if (p.flags & ~uint32_t(SLORR_ACCUMULATE | SLORR_VALUES_ONLY | SLORR_NO_GRAPH | SLORR_AUX |
+                          SLORR_DEFER_GRAD))
     throw std::invalid_argument("unknown flag bits");
+  if ((p.flags & SLORR_VALUES_ONLY) && (p.flags & SLORR_DEFER_GRAD))
+    throw std::invalid_argument("SLORR_VALUES_ONLY and SLORR_DEFER_GRAD exclude each other");
+  if (p.grad_dtype != SLORR_F32 && p.grad_dtype != SLORR_BF16)
+    throw std::domain_error("unsupported gradient dtype");
   if (p.coeffs.empty()) {
     p.coeffs.resize(size_t(p.iters) * 3);
     greedy_schedule(p.ell, p.degree, p.iters, p.coeffs.data());
@@ -276,10 +281,12 @@ void build_plan(Plan &p) {
     }
   }
   p.launches.push_back(plain(Op::Finalize, 1));
+  p.grad_launch = Launch{};
   if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {
     Launch l = plain(Op::Grad, p.prep.count, p.prep.first);
     l.which_x = p.iters & 1;                  // buffer the last update wrote
-    p.launches.push_back(l);
+    p.grad_launch = l;
+    if (!(p.flags & SLORR_DEFER_GRAD)) p.launches.push_back(l);
   }
 
   // MFMA work the launches execute (padded, symmetric tiles counted once)

@@ -58,6 +58,7 @@ struct Plan {
   double ell = 1e-3;
   float eps = 0.0f;
   uint32_t flags = 0;
+  slorr_dtype_t grad_dtype = SLORR_F32;
   std::vector<slorr_shape_t> shapes;
   std::vector<double> coeffs;          // iters x 3
   // derived
@@ -70,6 +71,7 @@ struct Plan {
   int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
   std::vector<Launch> launches;
+  Launch grad_launch{};                // the gradient epilogue (grid 0: nothing to write)
   double paper_flops = 0, mfma_flops = 0, weight_bytes = 0;
   // workspace layout (byte offsets)
   size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles = 0, off_chunks = 0, off_scal = 0,
@@ -84,10 +86,12 @@ struct Plan {
   void *staging_event[2] = {nullptr, nullptr};
   int staging_next = 0;
   bool dyn_valid = false;
+  bool state_ready = false;    // a forward run left X_T and s1, s2 in the workspace
   std::vector<DynDesc> dyn_cache;
   CallParams call_cache{};
 
   size_t elem_bytes() const { return dtype == SLORR_BF16 ? 2 : 4; }     // weights
+  size_t grad_bytes() const { return grad_dtype == SLORR_BF16 ? 2 : 4; }  // gradients
   size_t iter_bytes() const { return dtype == SLORR_BF16 ? 2 : 4; }     // X, A, B
   size_t dyn_bytes() const;                                            // dyn table + call params
 };

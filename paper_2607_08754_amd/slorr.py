@@ -13,7 +13,7 @@ from typing import Optional, Sequence, Tuple
 import numpy as np
 
 from . import _lib
-from ._lib import ACCUMULATE, AUX, NO_GRAPH, VALUES_ONLY, SlorrError, check, lib
+from ._lib import ACCUMULATE, AUX, DEFER_GRAD, NO_GRAPH, VALUES_ONLY, SlorrError, check, lib
 
 __all__ = ["Plan", "pe_coefficients", "SlorrError", "HOYER", "NUCLEAR"]
 
@@ -42,21 +42,31 @@ class Plan:
     plan(weights, grads) runs the forward + backward of the whole set on the
     current torch stream and returns the device tensor of values
     [L_0 .. L_{n-1}, sum] (plus n_hat and ||W||_F with aux=True).
+    With defer_grad=True the call writes no gradient; plan.grad(weights,
+    grads, scales) writes it afterwards from the state the call left.
+    grad_dtype is the element type of the gradient buffers ("f32" / "bf16").
     """
 
     def __init__(self, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", kind: str = HOYER,
                  iters: int = 6, degree: int = 5, ell: float = 1e-3, coeffs=None, eps: float = 0.0,
                  accumulate: bool = False, values_only: bool = False, graph: bool = True,
-                 aux: bool = False, device=None, create_workspace: bool = True):
+                 aux: bool = False, defer_grad: bool = False, grad_dtype: str = "f32",
+                 device=None, create_workspace: bool = True):
         self.shapes = [(int(r), int(c)) for r, c in shapes]
         self.n = len(self.shapes)
         self.dtype, self.kind, self.iters = dtype, kind, int(iters)
+        self.grad_dtype = grad_dtype
         self.flags = ((ACCUMULATE if accumulate else 0) | (VALUES_ONLY if values_only else 0)
-                      | (0 if graph else NO_GRAPH) | (AUX if aux else 0))
+                      | (0 if graph else NO_GRAPH) | (AUX if aux else 0)
+                      | (DEFER_GRAD if defer_grad else 0))
+        self.generation = 0          # forward calls enqueued so far
         self._c_shapes = _shapes_array(self.shapes)
+        if grad_dtype not in _DTYPE:
+            raise ValueError(f"grad_dtype must be one of {list(_DTYPE)}")
         opts = _lib.Options()
         lib().slorr_default_options(ctypes.byref(opts))
         opts.iters, opts.degree, opts.ell, opts.eps, opts.flags = int(iters), int(degree), float(ell), float(eps), self.flags
+        opts.grad_dtype = _DTYPE[grad_dtype]
         self._coeffs = None
         if coeffs is not None:
             c = np.ascontiguousarray(np.asarray(coeffs, dtype=np.float64).reshape(-1))
@@ -94,7 +104,7 @@ class Plan:
     def values_size(self) -> int:
         return (3 * self.n + 1) if (self.flags & AUX) else (self.n + 1)
 
-    def _marshal(self, weights, grads, out_vals, stream):
+    def _check_weights(self, weights):
         import torch
         if self.workspace is None:
             raise RuntimeError("plan has no workspace")
@@ -104,21 +114,27 @@ class Plan:
         for i, (w, s) in enumerate(zip(weights, self.shapes)):
             if tuple(w.shape) != s or w.dtype != want_dtype or not w.is_contiguous() or w.device != self.device:
                 raise ValueError(f"weights[{i}] must be a contiguous {want_dtype} {s} tensor on {self.device}")
-        want_grad = not (self.flags & VALUES_ONLY)
-        if want_grad:
-            if grads is None or len(grads) != self.n:
-                raise ValueError("grads: one fp32 tensor per weight is required")
-            for i, (g, s) in enumerate(zip(grads, self.shapes)):
-                if tuple(g.shape) != s or g.dtype != torch.float32 or not g.is_contiguous() or g.device != self.device:
-                    raise ValueError(f"grads[{i}] must be a contiguous float32 {s} tensor on {self.device}")
+        return (ctypes.c_void_p * max(1, self.n))(*[w.data_ptr() for w in weights])
+
+    def _grad_ptrs(self, grads):
+        import torch
+        want = torch.bfloat16 if self.grad_dtype == "bf16" else torch.float32
+        if grads is None or len(grads) != self.n:
+            raise ValueError(f"grads: one {want} tensor per weight is required")
+        for i, (g, s) in enumerate(zip(grads, self.shapes)):
+            if tuple(g.shape) != s or g.dtype != want or not g.is_contiguous() or g.device != self.device:
+                raise ValueError(f"grads[{i}] must be a contiguous {want} {s} tensor on {self.device}")
+        return (ctypes.c_void_p * max(1, self.n))(*[g.data_ptr() for g in grads])
+
+    def _marshal(self, weights, grads, out_vals, stream):
+        import torch
+        wp = self._check_weights(weights)
+        want_grad = not (self.flags & (VALUES_ONLY | DEFER_GRAD))
+        gp = self._grad_ptrs(grads) if want_grad else None
         if out_vals is None:
             out_vals = torch.empty(self.values_size(), dtype=torch.float32, device=self.device)
         elif out_vals.numel() < self.values_size() or out_vals.dtype != torch.float32:
             raise ValueError("out_vals too small or not float32")
-        wp = (ctypes.c_void_p * max(1, self.n))(*[w.data_ptr() for w in weights])
-        gp = None
-        if want_grad:
-            gp = (ctypes.c_void_p * max(1, self.n))(*[g.data_ptr() for g in grads])
         if stream is None:
             stream = torch.cuda.current_stream(self.device)
         return wp, gp, out_vals, stream
@@ -131,7 +147,48 @@ class Plan:
             check(lib().slorr_reg_fwd_bwd(self._handle, self.n, wp, self._c_shapes, _KIND[self.kind], self.iters,
                                           ctypes.c_void_p(out_vals.data_ptr()), gp, float(grad_scale),
                                           ctypes.c_void_p(stream.cuda_stream)), "slorr_reg_fwd_bwd")
+        self.generation += 1
         return out_vals
+
+    def grad(self, weights, grads, scales=None, grad_scale: float = 1.0, stream=None):
+        """Enqueue the gradient of the last forward call: grads[i] = g_i dL_i/dW_i
+        (added with accumulate=True), g_i = grad_scale * scales[i] with scales a
+        device float32 tensor of n entries (or grad_scale alone)."""
+        import torch
+        wp = self._check_weights(weights)
+        gp = self._grad_ptrs(grads)
+        sp = None
+        if scales is not None:
+            if scales.dtype != torch.float32 or scales.numel() != self.n or not scales.is_contiguous() \
+                    or scales.device != self.device:
+                raise ValueError(f"scales must be a contiguous float32 tensor of {self.n} entries on {self.device}")
+            sp = ctypes.c_void_p(scales.data_ptr())
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        with torch.cuda.device(self.device):
+            check(lib().slorr_reg_grad(self._handle, self.n, wp, self._c_shapes, _KIND[self.kind], self.iters,
+                                       gp, sp, float(grad_scale), ctypes.c_void_p(stream.cuda_stream)),
+                  "slorr_reg_grad")
+        return grads
+
+    def apply_update(self, weights, grads, step: float, steps=None, stream=None):
+        """Enqueue W_i <- W_i - s_i grads[i] in place, s_i = step * steps[i]
+        (steps: device float32 tensor of n entries) or step (App. E.2, Alg. 1)."""
+        import torch
+        wp = self._check_weights(weights)
+        gp = self._grad_ptrs(grads)
+        sp = None
+        if steps is not None:
+            if steps.dtype != torch.float32 or steps.numel() != self.n or not steps.is_contiguous() \
+                    or steps.device != self.device:
+                raise ValueError(f"steps must be a contiguous float32 tensor of {self.n} entries on {self.device}")
+            sp = ctypes.c_void_p(steps.data_ptr())
+        if stream is None:
+            stream = torch.cuda.current_stream(self.device)
+        with torch.cuda.device(self.device):
+            check(lib().slorr_decoupled_apply(self._handle, self.n, wp, self._c_shapes, gp, sp, float(step),
+                                              ctypes.c_void_p(stream.cuda_stream)), "slorr_decoupled_apply")
+        return weights
 
     def profiled(self, weights, grads=None, grad_scale: float = 1.0, out_vals=None, stream=None):
         """One call enqueued launch by launch with HIP events around every
@@ -146,6 +203,7 @@ class Plan:
                                                    self.iters, ctypes.c_void_p(out_vals.data_ptr()), gp,
                                                    float(grad_scale), ctypes.c_void_p(stream.cuda_stream),
                                                    ms, ops), "slorr_reg_fwd_bwd_profiled")
+        self.generation += 1
         return out_vals, [(_lib.OPS[ops[i]], float(ms[i])) for i in range(nl)]
 
     # ------------------------------------------------------------------ info

@@ -243,3 +243,52 @@ def test_binding_validates_in_python(L):
         p([np.zeros((4, 8))], None)
     assert p.info()["n"] == 1
     p.close()
+
+
+def test_deferred_gradient_and_apply_checks_before_device_use(L):
+    lib = L.lib()
+
+    def opts(**kw):
+        o = L.Options()
+        lib.slorr_default_options(ctypes.byref(o))
+        for k, v in kw.items():
+            setattr(o, k, v)
+        return o
+    assert opts().grad_dtype == L.F32
+    assert _plan(L, [(4, 8)], opts=opts(flags=L.VALUES_ONLY | L.DEFER_GRAD))[0] == L.ERR_INVALID_ARGUMENT
+    assert _plan(L, [(4, 8)], opts=opts(grad_dtype=5))[0] == L.ERR_UNSUPPORTED
+    # the deferred plan drops the gradient launch from its schedule
+    st, hn, _, _ = _plan(L, [(4, 8), (8, 4)])
+    st2, hd, _, shapes = _plan(L, [(4, 8), (8, 4)], opts=opts(flags=L.DEFER_GRAD, grad_dtype=L.BF16))
+    assert st == st2 == L.OK
+    ni, di = L.PlanInfo(), L.PlanInfo()
+    lib.slorr_plan_get_info(hn, ctypes.byref(ni))
+    lib.slorr_plan_get_info(hd, ctypes.byref(di))
+    assert di.launches == ni.launches - 1
+    w = (ctypes.c_void_p * 2)(0x20000, 0x30000)
+    vals = ctypes.c_void_p(0x10000)
+    # forward of a deferred plan needs no gradient buffers
+    assert lib.slorr_reg_fwd_bwd(hd, 2, w, shapes, 0, 6, vals, None, 1.0, None) == L.ERR_WORKSPACE
+    # bf16 gradients: 4x8 bf16 = 64 B, so these two buffers do not overlap
+    g = (ctypes.c_void_p * 2)(0x40000, 0x40040)
+    rg = lib.slorr_reg_grad
+    assert rg(None, 2, w, shapes, 0, 6, g, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert rg(hd, 3, w, shapes, 0, 6, g, None, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert rg(hd, 2, w, shapes, 0, 6, g, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert b"no forward state" in lib.slorr_last_error()
+    ap = lib.slorr_decoupled_apply
+    assert ap(None, 2, w, shapes, g, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert ap(hd, 1, w, shapes, g, None, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert ap(hd, 2, w, shapes, None, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert ap(hd, 2, w, shapes, g, ctypes.c_void_p(0x70002), 1.0, None) == L.ERR_INVALID_ARGUMENT
+    alias = (ctypes.c_void_p * 2)(0x20000, 0x50000)
+    assert ap(hd, 2, w, shapes, alias, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert ap(hd, 2, w, shapes, g, None, 1.0, None) == L.ERR_WORKSPACE
+    # the same buffers overlap once the gradients are fp32 (128 B each)
+    assert ap(hn, 2, w, shapes, g, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    # a values-only plan has no gradient to defer
+    st3, hv, _, _ = _plan(L, [(4, 8), (8, 4)], opts=opts(flags=L.VALUES_ONLY))
+    assert rg(hv, 2, w, shapes, 0, 6, g, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert b"values only" in lib.slorr_last_error()
+    for h in (hn, hd, hv):
+        lib.slorr_plan_destroy(h)
