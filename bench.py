@@ -87,7 +87,7 @@ def _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
     from oracle.slorr import fwd_bwd
     from workloads import widen
     table = pe_schedule(cfg.iters)
-    per_block = 4 if cfg.name.startswith("vit") else 1
+    per_block = cfg.block
     nblocks = cfg.n // per_block
     done, worst_v, worst_g = 0, 0.0, 0.0
     t0 = time.perf_counter()
@@ -121,6 +121,56 @@ def cpu_baseline(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
             "parity_on_sample": {"max_value_rel_err": wv, "max_grad_rel_err": wg}}
 
 
+SWEEPS = {
+    "vit": ["vit_ti", "vit_256", "vit_s", "vit_512", "vit_b16", "vit_b24", "vit_960_24", "vit_l16",
+            "vit_1152_28", "vit_h"],
+    "llm": ["llm135_paper", "llm560_paper", "llm560"],
+}
+
+
+def run_sweep(which, kind, steps, warmup):
+    """Weight-sets/s of each set of a sweep (graph replay, inputs resident);
+    one JSON line with a row per set."""
+    import numpy as np
+    import torch
+    from paper_2607_08754_amd import Plan
+    from workloads import CONFIGS, make_set
+    names = SWEEPS["vit"] + SWEEPS["llm"] if which == "all" else SWEEPS[which]
+    dev = torch.device("cuda:0")
+    rows = {}
+    for name in names:
+        cfg = CONFIGS[name]
+        arrs = make_set(name, 0)
+        W = [(torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if cfg.dtype == "bf16"
+              else torch.from_numpy(a)).to(dev) for a in arrs]
+        del arrs
+        G = [torch.empty(w.shape, dtype=torch.float32, device=dev) for w in W]
+        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, device=dev)
+        for _ in range(warmup):
+            plan(W, G)
+        torch.cuda.synchronize()
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        st.record()
+        for _ in range(steps):
+            plan(W, G)
+        en.record()
+        torch.cuda.synchronize()
+        ms = st.elapsed_time(en) / steps
+        peak = PEAK_TFLOPS[cfg.dtype]
+        tf = cfg.flops() / (ms * 1e-3) / 1e12
+        rows[name] = {"matrices": cfg.n, "params_M": round(cfg.params() / 1e6, 2),
+                      "paper_tflop_per_set": round(cfg.flops() / 1e12, 4), "ms_per_set": round(ms, 4),
+                      "weight_sets_per_s": round(1000.0 / ms, 2), "paper_tflops": round(tf, 1),
+                      "frac_of_peak": round(tf / peak, 4), "mfma_flops_per_set": plan.info()["mfma_flops"]}
+        print(f"[sweep] {name}: {ms:.3f} ms/set, {tf:.0f} TFLOP/s (paper count)", file=sys.stderr, flush=True)
+        plan.close()
+        del W, G, plan
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": f"SLORR-{kind} fwd+bwd per weight set across model scales",
+                      "unit": "ms/set", "steps": steps, "warmup": warmup, "data": "synthetic",
+                      "sweep": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -134,6 +184,9 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
+    ap.add_argument("--sweep", choices=["vit", "llm", "all"], default=None,
+                    help="time every set of a scaling sweep (App. D ViT configurations, App. F LLM "
+                         "shapes) instead of the headline workload; prints one JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the hot path has no "
@@ -144,6 +197,10 @@ def main():
     import torch
     from paper_2607_08754_amd import Plan
     from workloads import CONFIGS, make_set
+
+    if args.sweep:
+        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)))
+        return
 
     if args.calibrate_copy:
         n = args.calibrate_copy << 20

@@ -23,7 +23,7 @@ from typing import Callable, List, Sequence, Tuple
 
 import numpy as np
 
-__all__ = ["WeightSet", "CONFIGS", "make_set", "widen", "f32_to_bf16_bits",
+__all__ = ["WeightSet", "CONFIGS", "VIT_SWEEP", "make_set", "widen", "f32_to_bf16_bits",
            "bf16_bits_to_f32", "gaussian", "config_shapes"]
 
 Shape = Tuple[int, int]
@@ -107,6 +107,7 @@ class WeightSet:
     shapes: List[Shape]
     gen: Callable = field(repr=False, default=None)
     note: str = ""
+    block: int = 1                # matrices per repeated unit (transformer block / layer)
 
     @property
     def n(self) -> int:
@@ -148,6 +149,24 @@ def _llm_shapes():
     return out
 
 
+def _llama_shapes(layers: int, hidden: int, inter: int):
+    # Llama-like block with full multi-head attention (App. F table of model
+    # sizes): q, k, v, o (hidden x hidden), SwiGLU gate and up (inter x hidden)
+    # and down (hidden x inter); every linear layer of the block is regularized
+    out = []
+    for _ in range(layers):
+        out += [(hidden, hidden)] * 4 + [(inter, hidden), (inter, hidden), (hidden, inter)]
+    return out
+
+
+# ViT scaling sweep (App. D, table of ViT configurations): name -> (embed dim,
+# depth); patch 16 and MLP ratio 4 throughout. ViT-B and ViT-L are the
+# vit_b16 / vit_l16 sets.
+VIT_SWEEP = {"vit_ti": (192, 12), "vit_256": (256, 12), "vit_s": (384, 12), "vit_512": (512, 12),
+             "vit_b16": (768, 12), "vit_b24": (768, 24), "vit_960_24": (960, 24), "vit_l16": (1024, 24),
+             "vit_1152_28": (1152, 28), "vit_h": (1280, 32)}
+
+
 CONFIGS = {
     "tiny": WeightSet("tiny", "f32", 5, ("hoyer", "nuclear"), _tiny_shapes(),
                       _gen_gauss(lambda s: 1.0 / 16.0),
@@ -159,15 +178,29 @@ CONFIGS = {
     "vit_b16": WeightSet("vit_b16", "bf16", 6, ("hoyer", "nuclear"), _vit_shapes(12, 768),
                          _gen_vit_b,
                          "12 blocks qkv/proj/fc1/fc2; N(0, 0.02^2) + rank-16 term of "
-                         "Frobenius norm 0.3 ||G||_F"),
+                         "Frobenius norm 0.3 ||G||_F", block=4),
     "vit_l16": WeightSet("vit_l16", "bf16", 6, ("hoyer", "nuclear"), _vit_shapes(24, 1024),
                          _gen_vit_l,
-                         "24 blocks qkv/proj/fc1/fc2; Haar U, V, sigma_i ~ i^-1/2, RMS 0.02"),
+                         "24 blocks qkv/proj/fc1/fc2; Haar U, V, sigma_i ~ i^-1/2, RMS 0.02", block=4),
     "llm560": WeightSet("llm560", "bf16", 6, ("hoyer",), _llm_shapes(),
                         _gen_gauss(lambda s: 0.02),
                         "24 layers GQA q/k/v/o + SwiGLU gate/up/down at hidden 1536; "
-                        "N(0, 0.02^2)"),
+                        "N(0, 0.02^2)", block=7),
+    "llm135_paper": WeightSet("llm135_paper", "bf16", 6, ("hoyer",), _llama_shapes(12, 768, 2048),
+                              _gen_gauss(lambda s: 0.02),
+                              "12 layers q/k/v/o 768^2 + SwiGLU gate/up 2048x768, down 768x2048; "
+                              "N(0, 0.02^2)", block=7),
+    "llm560_paper": WeightSet("llm560_paper", "bf16", 6, ("hoyer",), _llama_shapes(24, 1280, 3456),
+                              _gen_gauss(lambda s: 0.02),
+                              "24 layers q/k/v/o 1280^2 + SwiGLU gate/up 3456x1280, down 1280x3456; "
+                              "N(0, 0.02^2)", block=7),
 }
+for _name, (_d, _depth) in VIT_SWEEP.items():
+    if _name not in CONFIGS:
+        CONFIGS[_name] = WeightSet(_name, "bf16", 6, ("hoyer",), _vit_shapes(_depth, _d), _gen_vit_b,
+                                   f"{_depth} blocks qkv/proj/fc1/fc2 at embed dim {_d}; "
+                                   "N(0, 0.02^2) + rank-16 term of Frobenius norm 0.3 ||G||_F", block=4)
+
 
 
 def config_shapes(name: str) -> List[Shape]:
