@@ -212,8 +212,9 @@ typedef enum {
   SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
   SLORR_OP_UPDATE = 5,    /* X = a_t X + B X                              */
   SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
-  SLORR_OP_FINALIZE = 7,  /* values, set sum, gradient factors            */
-  SLORR_OP_GRAD = 8       /* gradient epilogue                            */
+  SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
+  SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
+  SLORR_OP_SETSUM = 9     /* the set total, summed in index order         */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the

@@ -132,6 +132,24 @@ __device__ __forceinline__ double dot_w(const Tw *w, const float (&v)[8], int n)
   return s;
 }
 
+// 8 consecutive weights as loaded (bf16 bits or fp32), for a load issued
+// ahead of its use.
+template <typename Tw> struct WChunk;
+template <> struct WChunk<uint16_t> {
+  typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+  u16x8 h;
+  __device__ __forceinline__ void load(const uint16_t *p) { h = *reinterpret_cast<const u16x8 *>(p); }
+  __device__ __forceinline__ float get(int j) const { return __uint_as_float(uint32_t(h[j]) << 16); }
+};
+template <> struct WChunk<float> {
+  float4v a, b;
+  __device__ __forceinline__ void load(const float *p) {
+    a = reinterpret_cast<const float4v *>(p)[0];
+    b = reinterpret_cast<const float4v *>(p)[1];
+  }
+  __device__ __forceinline__ float get(int j) const { return j < 4 ? a[j] : b[j - 4]; }
+};
+
 // 8 consecutive values of type T from global memory (16-byte aligned).
 template <typename T>
 __device__ __forceinline__ void load8(const T *p, float (&v)[8]) {
@@ -331,15 +349,65 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   double tsum = 0.0;
   const Tw *W = (MODE == kLast) ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
 
+  // Last: the weights each lane multiplies into the trace are known before
+  // the accumulators are staged, so they are loaded one 32-row block ahead
+  // (two register buffers) instead of being waited for task by task. Task t
+  // of a lane: row phase (wide W) row / column group, column phase (tall W)
+  // row group / column; both phases have NTASK tasks per lane.
+  constexpr int NTASK = 32 * CG / 64;
+  static_assert(NTASK * 64 == 32 * CG && NTASK * 64 == WTN * 4, "epilogue task split");
+  WChunk<Tw> wpre[2][NTASK];
+  bool wfull[2][NTASK];
+  auto wtask = [&](int i, int t, const Tw *&ptr, int &nv) -> bool {
+    const int task = lane + 64 * t;
+    const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
+    if (!d.tall) {                     // canonical (m, n) = W[m][n]
+      const int grow = grow0 + task / CG, gcol = gcol0 + (task % CG) * 8;
+      ptr = W + size_t(grow) * d.cols + gcol;
+      nv = min(8, d.Q - gcol);
+      return grow < d.P && gcol < d.Q;
+    }
+    const int orow = gcol0 + (task >> 2), ocol = grow0 + (task & 3) * 8;   // W[n][m]
+    ptr = W + size_t(orow) * d.cols + ocol;
+    nv = min(8, d.P - ocol);
+    return orow < d.Q && ocol < d.P;
+  };
+  auto wprefetch = [&](int i, int b) {
+#pragma unroll
+    for (int t = 0; t < NTASK; ++t) {
+      const Tw *ptr;
+      int nv;
+      const bool ok = wtask(i, t, ptr, nv);
+      wfull[b][t] = ok && nv == 8 && (reinterpret_cast<uintptr_t>(ptr) & 15) == 0;
+      if (wfull[b][t]) wpre[b][t].load(ptr);
+    }
+  };
+  // sum_j v[j] * W(task)[j] for task t of block i (prefetched or direct)
+  auto wdot = [&](int i, int b, int t, const float (&v)[8]) -> double {
+    const Tw *ptr;
+    int nv;
+    if (!wtask(i, t, ptr, nv)) return 0.0;
+    if (!wfull[b][t]) return dot_w(ptr, v, nv);
+    double s = 0.0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wpre[b][t].get(j));
+    return s;
+  };
+  if constexpr (MODE == kLast) wprefetch(0, 0);
+
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
+    if constexpr (MODE == kLast)
+      if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) ep[(8 * (r >> 2) + 4 * lk + (r & 3)) * P + j * 32 + lr] = acc[i][j][r];
     __syncthreads();
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
-    for (int task = lane; task < 32 * CG; task += 64) {
+#pragma unroll
+    for (int t = 0; t < NTASK; ++t) {
+      const int task = lane + 64 * t;
       const int row = task / CG, cg = task % CG;
       float4v *e = reinterpret_cast<float4v *>(ep + row * P + cg * 8);
       float v[8];
@@ -376,9 +444,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         if (MODE == kLast) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
-          // wide W: canonical (m, n) = W[m][n], contiguous along the row
-          if (!d.tall && grow < d.P && gcol < d.Q)
-            tsum += dot_w(W + size_t(grow) * d.cols + gcol, v, min(8, d.Q - gcol));
+          if (!d.tall) tsum += wdot(i, i & 1, t, v);
         }
       }
       if (colwise) {
@@ -395,7 +461,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     __syncthreads();
     if (colwise) {
       // transpose: output row = this tile's column, 8 consecutive source rows
-      for (int task = lane; task < WTN * 4; task += 64) {
+#pragma unroll
+      for (int t = 0; t < NTASK; ++t) {
+        const int task = lane + 64 * t;
         const int rg = task & 3, col = task >> 2;
         float v[8];
 #pragma unroll
@@ -406,10 +474,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         } else if (MODE == kPoly) {
           store8(Bm + size_t(orow) * d.Pp + ocol, v);
         } else if (MODE == kLast) {
-          // tall W: canonical (m, n) = W[n][m]; here n = orow, m = ocol + j,
-          // contiguous along W's row
-          if (orow < d.Q && ocol < d.P)
-            tsum += dot_w(W + size_t(orow) * d.cols + ocol, v, min(8, d.P - ocol));
+          tsum += wdot(i, i & 1, t, v);       // tall W (colwise only for tall)
         }
       }
       __syncthreads();

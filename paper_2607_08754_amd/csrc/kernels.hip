@@ -13,8 +13,9 @@
 //                Last    X_T = a X + B X with the trace partials of
 //                        sum(W * P), P = X_T (Sec. 3 "Computing the nuclear
 //                        and Frobenius norms")
-//   k_finalize values L_i, the set sum in index order, gradient factors
+//   k_finalize values L_i and gradient factors, one block per matrix
 //              (Sec. 3 definitions; Eq. SLORR_grads; Listing 1)
+//   k_setsum   the set total in index order (Sec. 3, L summed over the set)
 //   k_grad     grad = g (s1 P - s2 W)  (Hoyer) or g P (nuclear) from the last
 //              iterate, in W's orientation, optionally accumulated into the
 //              caller's buffer (App. E.3)
@@ -241,49 +242,59 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
 // Values and gradient factors; one wave per matrix reduces its trace
 // partials (lane-strided, fixed butterfly). One block; the set sum is taken
 // by thread 0 in index order.
-__global__ __launch_bounds__(kThreads) void k_finalize(const MatDesc *__restrict__ mats,
-                                                       Scalars *sc,
-                                                       const double *__restrict__ tpart,
-                                                       const CallParams *__restrict__ call,
-                                                       int n, int kind, int aux) {
+// Values and gradient factors: one 64-thread block per matrix, all matrices
+// at once. The trace partials of the matrix are summed by the wave (fixed
+// butterfly order).
+__global__ __launch_bounds__(64) void k_finalize(const MatDesc *__restrict__ mats, Scalars *sc,
+                                                 const double *__restrict__ tpart,
+                                                 const CallParams *__restrict__ call, int n, int kind,
+                                                 int aux) {
+  const int i = blockIdx.x, lane = threadIdx.x;
   float *out = call->out_vals;
-  const int lane = threadIdx.x & 63;
-  for (int i = threadIdx.x >> 6; i < n; i += kThreads / 64) {
-    const MatDesc d = mats[i];
-    double nh = 0.0;
-    for (int s = d.trace_begin + lane; s < d.trace_end; s += 64) nh += tpart[s];
-    nh = wave_sum(nh);
-    if (lane != 0) continue;
-    const double fe = d.empty ? 0.0 : sc[i].feps;
-    double L = 0.0, s1 = 0.0, s2 = 0.0;
-    if (d.empty || fe == 0.0) {
-      nh = 0.0;
-    } else if (kind == SLORR_HOYER) {
-      const double r = nh / fe;           // n / (f + eps)
-      L = r * r;
-      s1 = 2.0 * nh / (fe * fe);          // 2 r / (f + eps)
-      s2 = 2.0 * nh * nh / (fe * fe * fe * fe);  // 2 r n / (f + eps)^3
-    } else {
-      L = nh;
-      s1 = 1.0;
-    }
-    sc[i].nhat = nh;
-    sc[i].value = L;
-    sc[i].s1 = s1;
-    sc[i].s2 = s2;
-    out[i] = float(L);
-    if (aux) {
-      out[n + 1 + i] = float(nh);
-      out[2 * n + 1 + i] = d.empty ? 0.0f : float(sc[i].f);
-    }
+  const MatDesc d = mats[i];
+  double nh = 0.0;
+  for (int s = d.trace_begin + lane; s < d.trace_end; s += 64) nh += tpart[s];
+  nh = wave_sum(nh);
+  if (lane != 0) return;
+  const double fe = d.empty ? 0.0 : sc[i].feps;
+  double L = 0.0, s1 = 0.0, s2 = 0.0;
+  if (d.empty || fe == 0.0) {
+    nh = 0.0;
+  } else if (kind == SLORR_HOYER) {
+    const double r = nh / fe;           // n / (f + eps)
+    L = r * r;
+    s1 = 2.0 * nh / (fe * fe);          // 2 r / (f + eps)
+    s2 = 2.0 * nh * nh / (fe * fe * fe * fe);  // 2 r n / (f + eps)^3
+  } else {
+    L = nh;
+    s1 = 1.0;
   }
-  __threadfence_block();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double tot = 0.0;
-    for (int i = 0; i < n; ++i) tot += sc[i].value;
-    out[n] = float(tot);
+  sc[i].nhat = nh;
+  sc[i].value = L;
+  sc[i].s1 = s1;
+  sc[i].s2 = s2;
+  out[i] = float(L);
+  if (aux) {
+    out[n + 1 + i] = float(nh);
+    out[2 * n + 1 + i] = d.empty ? 0.0f : float(sc[i].f);
   }
+}
+
+// The set total sum_i L_i, added in index order (fp64): the values are
+// staged in LDS a chunk at a time and one thread adds them.
+__global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
+                                                 const CallParams *__restrict__ call, int n) {
+  __shared__ double v[1024];
+  double tot = 0.0;
+  for (int base = 0; base < n; base += 1024) {
+    const int m = min(1024, n - base);
+    if (int(threadIdx.x) < m) v[threadIdx.x] = sc[base + threadIdx.x].value;
+    __syncthreads();
+    if (threadIdx.x == 0)
+      for (int j = 0; j < m; ++j) tot += v[j];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) call->out_vals[n] = float(tot);
 }
 
 // ---------------------------------------------------------------- gradient
@@ -474,8 +485,11 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         break;
       }
       case Op::Finalize:
-        hipLaunchKernelGGL(k_finalize, grid, block, 0, s, mats, sc, trace, call, p.n, int(p.kind),
+        hipLaunchKernelGGL(k_finalize, grid, dim3(64), 0, s, mats, sc, trace, call, p.n, int(p.kind),
                            (p.flags & SLORR_AUX) ? 1 : 0);
+        break;
+      case Op::SetSum:
+        hipLaunchKernelGGL(k_setsum, dim3(1), dim3(1024), 0, s, sc, call, p.n);
         break;
       case Op::Grad:
         launch_grad<Tw, Tx>(p, l, s);

@@ -280,7 +280,8 @@ void build_plan(Plan &p) {
         gemm(op, p.pq[cfg], cfg, wx, 1, 0, float(b / sa), float(a), 0.0f);
     }
   }
-  p.launches.push_back(plain(Op::Finalize, 1));
+  if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
+  p.launches.push_back(plain(Op::SetSum, 1));
   p.grad_launch = Launch{};
   if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {
     Launch l = plain(Op::Grad, p.prep.count, p.prep.first);

@@ -23,8 +23,9 @@ enum class Op : int {
   Poly = SLORR_OP_POLY,          // B = b A + c A A
   Update = SLORR_OP_UPDATE,      // X' = a X + B X        (or a X + b A X when c = 0)
   Last = SLORR_OP_LAST,          // final update: P, trace partials
-  Finalize = SLORR_OP_FINALIZE,  // values, set sum, gradient coefficients
-  Grad = SLORR_OP_GRAD           // grad = c1 P - c2 W   (original orientation)
+  Finalize = SLORR_OP_FINALIZE,  // values and gradient factors, one block per matrix
+  Grad = SLORR_OP_GRAD,          // grad = g (s1 P - s2 W)   (original orientation)
+  SetSum = SLORR_OP_SETSUM       // set total in index order
 };
 
 // GEMM block-tile configurations (kernel template instances).
