@@ -214,7 +214,8 @@ typedef enum {
   SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
-  SLORR_OP_SETSUM = 9     /* the set total, summed in index order         */
+  SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
+  SLORR_OP_GRAM_REDUCE = 10 /* sum of split-K Gram partials, A = X X^T     */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the

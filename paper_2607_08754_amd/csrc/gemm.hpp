@@ -67,6 +67,7 @@ struct GemmArgs {
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
   float alpha, beta, gamma, inv_sx;
+  float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
 };
 
 template <int BM, int BN, int WGM, int WGN>
@@ -205,6 +206,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 
   const Tile tile = args.tiles[blockIdx.x];
   if (tile.mat < 0) return;      // padding of the XCD-ordered list (whole block)
+  // a Gram part (split K) covers k in [k0, k1) and stores its raw fp32 partial
+  const bool part = MODE == kGram && tile.k1 > 0;
   const MatDesc d = args.mats[tile.mat];
   const int m0 = tile.tm * BM, n0 = tile.tn * BN;
   T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
@@ -217,6 +220,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   int lda, ldb, K;
   if (MODE == kGram) {
     Ap = Xc; Bp = Xc; lda = ldb = d.Qp; K = d.Qp;
+    if (part) {
+      Ap += tile.k0;
+      Bp += tile.k0;
+      K = tile.k1 - tile.k0;
+    }
   } else if (MODE == kPoly) {
     Ap = Am; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
   } else {
@@ -344,7 +352,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
   const float alpha = args.alpha, beta = args.beta;
-  const bool mirror = (MODE == kGram || MODE == kPoly) && tile.tm != tile.tn;
+  const bool mirror = (MODE == kGram || MODE == kPoly) && tile.tm != tile.tn && !part;
   const bool colwise = mirror || (MODE == kLast && d.tall);
   double tsum = 0.0;
   const Tw *W = (MODE == kLast) ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
@@ -421,9 +429,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       }
       const int grow = grow0 + row, gcol = gcol0 + cg * 8;
       if (MODE == kGram) {
+        if (part) {
+          store8(args.gpart + size_t(tile.slot) * (BM * BN) + size_t(grow - m0) * BN + (gcol - n0), v);
+        } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] *= alpha;
-        store8(Am + size_t(grow) * d.Pp + gcol, v);
+          for (int j = 0; j < 8; ++j) v[j] *= alpha;
+          store8(Am + size_t(grow) * d.Pp + gcol, v);
+        }
       } else if (MODE == kPoly) {
         float in[8];
         load8(Am + size_t(grow) * d.Pp + gcol, in);

@@ -16,6 +16,8 @@
 //   k_finalize values L_i and gradient factors, one block per matrix
 //              (Sec. 3 definitions; Eq. SLORR_grads; Listing 1)
 //   k_setsum   the set total in index order (Sec. 3, L summed over the set)
+//   k_gram_reduce  A = X X^T from split-K partial tiles (sets with few, long
+//              Gram tiles), fixed summation order
 //   k_grad     grad = g (s1 P - s2 W)  (Hoyer) or g P (nuclear) from the last
 //              iterate, in W's orientation, optionally accumulated into the
 //              caller's buffer (App. E.3)
@@ -297,6 +299,53 @@ __global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
   if (threadIdx.x == 0) call->out_vals[n] = float(tot);
 }
 
+// Split-K Gram: A tile = alpha * (sum of its fp32 partials, in part order),
+// stored with its transpose for off-diagonal tiles. kRedStripes blocks per
+// tile, each a stripe of rows; the stripe passes through LDS so that the
+// transposed store is row-contiguous too.
+template <typename Tx>
+__global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict__ tiles,
+                                                          const MatDesc *__restrict__ mats,
+                                                          char *__restrict__ ws,
+                                                          const float *__restrict__ gpart, float alpha) {
+  constexpr int R = kTile / kRedStripes;          // rows per stripe
+  __shared__ float t[R][kTile + 1];
+  const Tile e = tiles[blockIdx.x / kRedStripes];
+  const int stripe = blockIdx.x % kRedStripes;
+  const MatDesc d = mats[e.mat];
+  Tx *A = reinterpret_cast<Tx *>(ws + d.a);
+  const int m0 = e.tm * kTile + stripe * R, n0 = e.tn * kTile;
+  const float *src = gpart + size_t(e.slot) * (kTile * kTile) + stripe * R * kTile;
+  for (int q = threadIdx.x; q < R * kTile / 4; q += kThreads) {
+    float4v acc = reinterpret_cast<const float4v *>(src)[q];
+    for (int s = 1; s < e.parts; ++s) {
+      const float4v v = reinterpret_cast<const float4v *>(src + size_t(s) * (kTile * kTile))[q];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] += v[j];
+    }
+    const int r = (4 * q) / kTile, c = (4 * q) % kTile;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) t[r][c + j] = alpha * acc[j];
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < R * kTile / 8; q += kThreads) {
+    const int r = (8 * q) / kTile, c = (8 * q) % kTile;
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = t[r][c + j];
+    put8(A + size_t(m0 + r) * d.Pp + n0 + c, 8, v);
+  }
+  if (e.tm != e.tn) {                 // the transpose: R consecutive columns per output row
+    for (int q = threadIdx.x; q < R * kTile / 8; q += kThreads) {
+      const int c = (8 * q) / R, r = (8 * q) % R;     // output row n0 + c, columns m0 + r ..
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = t[r + j][c];
+      put8(A + size_t(n0 + c) * d.Pp + m0 + r, 8, v);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- gradient
 
 // Gradient in W's own orientation from the last iterate X_T (canonical,
@@ -478,6 +527,7 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.gamma = l.gamma;
         a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
+        a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
         if (l.cfg == kCfg256)
           launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s);
         else
@@ -487,6 +537,10 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
       case Op::Finalize:
         hipLaunchKernelGGL(k_finalize, grid, dim3(64), 0, s, mats, sc, trace, call, p.n, int(p.kind),
                            (p.flags & SLORR_AUX) ? 1 : 0);
+        break;
+      case Op::GramReduce:
+        hipLaunchKernelGGL((k_gram_reduce<Tx>), grid, block, 0, s, tiles + l.tile_first, mats, ws,
+                           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha);
         break;
       case Op::SetSum:
         hipLaunchKernelGGL(k_setsum, dim3(1), dim3(1024), 0, s, sc, call, p.n);

@@ -17,6 +17,7 @@ constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
 constexpr int kChunk = 8192;     // elements per block in the norm and gradient kernels
 constexpr int kThreads = 256;    // threads per block of the non-GEMM kernels
 constexpr int kXcds = 8;         // XCDs of an MI355X; workgroup b runs on XCD b % 8
+constexpr int kRedStripes = 4;   // split-K Gram reduce: blocks (row stripes) per tile
 
 // Power-of-two operand scales of the fp16 iterate (bf16 weights). With the
 // input normalised by ||W||_F every singular value of X stays <= u_t <= 2, so
@@ -50,8 +51,10 @@ struct CallParams {            // per call
   int32_t pad;
 };
 
-struct Tile {                  // one GEMM output tile / one prep tile
+struct Tile {                  // one GEMM output tile / one prep tile / one Gram part
   int32_t mat, tm, tn, slot;   // mat < 0: padding entry, the block exits at once
+  int32_t k0, k1;              // Gram part: its k range [k0, k1); k1 = 0: all of K
+  int32_t parts, pad;          // Gram reduce entry: partials slot .. slot + parts - 1
 };
 
 struct Chunk {                 // a contiguous run of a matrix's elements

@@ -16,6 +16,8 @@ constexpr int64_t kMaxShort = 16384;
 constexpr int64_t kMaxLong = 1 << 20;
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 constexpr int64_t kMinBigTiles = 2 * 256;   // two 256-tiles per CU (256 CUs)
+constexpr int64_t kMinGramUnits = 2 * 256;  // Gram blocks wanted per launch (two per CU)
+constexpr int kMaxGramParts = 16;           // k parts per Gram tile at most
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
@@ -168,6 +170,49 @@ void build_plan(Plan &p) {
     }
     p.pp[cfg] = emit(std::move(jobs));
   }
+  // Split-K Gram. A set with few Gram tiles (small P) but long K = Qp would
+  // leave most CUs idle: every tile's k range is cut into parts (multiples of
+  // kTile) so that the launch has about kMinGramUnits blocks; each part writes
+  // an fp32 partial tile, and a reduce launch adds the parts in order.
+  p.gsplit = TileRange{};
+  p.gred = TileRange{};
+  p.gram_parts = 0;
+  {
+    int64_t ntiles = 0;
+    for (int i : order)
+      if (pp_cfg(p.mats[i]) == kCfg128) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
+    if (ntiles > 0 && ntiles < kMinGramUnits) {
+      const int want = int(std::max<int64_t>(1, std::min<int64_t>(kMaxGramParts, kMinGramUnits / ntiles)));
+      std::vector<Job> jobs;
+      std::vector<Tile> reds;
+      for (int i : order) {
+        const MatDesc &d = p.mats[i];
+        if (pp_cfg(d) != kCfg128) continue;
+        const int nblk = d.Qp / kTile;                     // k blocks of kTile
+        const int per = (nblk + std::min(want, nblk) - 1) / std::min(want, nblk);
+        const int parts = (nblk + per - 1) / per;
+        Job j{i, double(per * kTile), {}};
+        const int nt = d.Pp / kTile;
+        for (int tm = 0; tm < nt; ++tm)
+          for (int tn = tm; tn < nt; ++tn) {
+            Tile r{i, tm, tn, p.gram_parts};
+            r.parts = parts;
+            reds.push_back(r);
+            for (int q = 0; q < parts; ++q) {
+              Tile t{i, tm, tn, p.gram_parts++};
+              t.k0 = q * per * kTile;
+              t.k1 = std::min(nblk, (q + 1) * per) * kTile;
+              j.tiles.push_back(t);
+            }
+          }
+        jobs.push_back(std::move(j));
+      }
+      p.gsplit = emit(std::move(jobs));
+      p.gred.first = int32_t(p.tiles.size());
+      p.tiles.insert(p.tiles.end(), reds.begin(), reds.end());
+      p.gred.count = int32_t(reds.size());
+    }
+  }
   // Update tiles; each owns one trace-partial slot, contiguous per matrix
   int32_t slot = 0;
   for (int cfg = 0; cfg < kNumCfg; ++cfg) {
@@ -216,6 +261,7 @@ void build_plan(Plan &p) {
   p.off_scal = take(sizeof(Scalars) * p.n);
   p.off_sumsq = take(sizeof(double) * p.chunks.size());
   p.off_trace = take(sizeof(double) * p.trace_slots);
+  p.off_gpart = take(sizeof(float) * size_t(kTile) * kTile * size_t(p.gram_parts));
   p.off_static_end = off;
   const size_t es = p.iter_bytes();
   for (int i = 0; i < p.n; ++i) {
@@ -262,8 +308,15 @@ void build_plan(Plan &p) {
     const int32_t wx = t & 1;
     const bool quintic = c != 0.0;
     // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
-    for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
-      gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, 0, float(sa / (double(sx) * sx)), 0.0f, 0.0f);
+    const float galpha = float(sa / (double(sx) * sx));
+    if (p.gsplit.count) {
+      gemm(Op::Gram, p.gsplit, kCfg128, wx, 0, 0, galpha, 0.0f, 0.0f);     // fp32 partials
+      Launch l = plain(Op::GramReduce, p.gred.count * kRedStripes, p.gred.first);
+      l.alpha = galpha;
+      p.launches.push_back(l);
+    } else {
+      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg) gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, 0, galpha, 0.0f, 0.0f);
+    }
     const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
     if (quintic) {
       // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
@@ -299,7 +352,9 @@ void build_plan(Plan &p) {
       const int mi = p.tiles[l.tile_first + k].mat;
       if (mi < 0) continue;
       const MatDesc &d = p.mats[mi];
-      p.mfma_flops += 2.0 * ts * ts * (l.op == Op::Gram ? d.Qp : d.Pp);
+      const Tile &tl = p.tiles[l.tile_first + k];
+      const double kk = l.op == Op::Gram ? (tl.k1 > 0 ? double(tl.k1 - tl.k0) : double(d.Qp)) : double(d.Pp);
+      p.mfma_flops += 2.0 * ts * ts * kk;
     }
   }
 }

@@ -25,7 +25,8 @@ enum class Op : int {
   Last = SLORR_OP_LAST,          // final update: P, trace partials
   Finalize = SLORR_OP_FINALIZE,  // values and gradient factors, one block per matrix
   Grad = SLORR_OP_GRAD,          // grad = g (s1 P - s2 W)   (original orientation)
-  SetSum = SLORR_OP_SETSUM       // set total in index order
+  SetSum = SLORR_OP_SETSUM,      // set total in index order
+  GramReduce = SLORR_OP_GRAM_REDUCE  // A = sum of the split-K Gram partials
 };
 
 // GEMM block-tile configurations (kernel template instances).
@@ -69,6 +70,8 @@ struct Plan {
   TileRange pp[kNumCfg];                     // P x P outputs (gram, poly), per GemmCfg
   TileRange pq[kNumCfg];                     // P x Q outputs (update, last), per GemmCfg
   TileRange prep;                      // prep tiles over Pp x Qp
+  TileRange gsplit, gred;              // split-K Gram: part entries, reduce entries
+  int32_t gram_parts = 0;              // fp32 partial tiles in the workspace
   int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
   std::vector<Launch> launches;
@@ -76,7 +79,7 @@ struct Plan {
   double paper_flops = 0, mfma_flops = 0, weight_bytes = 0;
   // workspace layout (byte offsets)
   size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles = 0, off_chunks = 0, off_scal = 0,
-         off_sumsq = 0, off_trace = 0, off_static_end = 0, ws_bytes = 0;
+         off_sumsq = 0, off_trace = 0, off_gpart = 0, off_static_end = 0, ws_bytes = 0;
   // runtime state (owned by the API layer)
   void *ws = nullptr;
   int device = -1;

@@ -292,3 +292,30 @@ def test_deferred_gradient_and_apply_checks_before_device_use(L):
     assert b"values only" in lib.slorr_last_error()
     for h in (hn, hd, hv):
         lib.slorr_plan_destroy(h)
+
+
+def test_split_k_gram_plan(L):
+    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch
+    per step; the parts cover every k exactly once (same executed MFMA work
+    as one pass per tile). Sets with enough tiles are not split."""
+    def facts(shapes):
+        st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
+        assert st == L.OK
+        info = L.PlanInfo()
+        L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+        L.lib().slorr_plan_destroy(h)
+        return info
+    shapes = [(256, 4096), (4096, 256), (384, 2944)]           # 3 + 3 + 6 Gram tiles
+    info = facts(shapes)
+    T = 6
+    assert info.launches == 3 + 4 * T + 3                    # gram parts, reduce, poly, update
+    want = 0.0
+    for m, n in shapes:
+        P, Q = min(m, n), max(m, n)
+        Pp, Qp = -(-P // 128) * 128, -(-Q // 128) * 128
+        nt = Pp // 128
+        tri = nt * (nt + 1) / 2 * 128.0 * 128.0
+        want += T * (2 * tri * Qp + 2 * tri * Pp + 2.0 * Pp * Pp * Qp)
+    assert info.mfma_flops == pytest.approx(want, rel=1e-12)
+    big = facts(CONFIGS["vit_b16"].shapes)
+    assert big.launches == 3 + 3 * 6 + 3

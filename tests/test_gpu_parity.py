@@ -87,6 +87,17 @@ def test_ragged_shapes(dtype, kind):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_split_k_gram_long_rows(dtype):
+    """Few Gram tiles with long k ranges: the split-K Gram (parts of unequal
+    length when Qp / 128 is not a multiple of the part count) and its reduce."""
+    shapes = [(200, 5000), (2600, 96), (130, 3000)]
+    arrs = [gaussian(s, seed=101, std=0.03, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+    vals, grads, _ = run_gpu(arrs, dtype, "hoyer", 6)
+    refs = run_oracle(arrs, dtype, "hoyer", 6)
+    compare(vals, grads, refs, "hoyer", dtype, label=f"split-K {dtype}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_empty_and_zero_matrices(dtype):
     import torch
     from paper_2607_08754_amd import Plan
