@@ -156,18 +156,38 @@ __global__ __launch_bounds__(kThreads) void k_sumsq(const Chunk *__restrict__ ch
   constexpr int V = 16 / sizeof(Tw);
   typedef Tw vec_t __attribute__((ext_vector_type(V)));
   double acc = 0.0;
-  const int nvec = ch.len / V;
-  for (int i = threadIdx.x; i < nvec; i += kThreads) {
-    const vec_t v = reinterpret_cast<const vec_t *>(w)[i];
+  if (ch.len == kChunk) {
+    // full chunk: the thread's loads are issued in batches of 8
+    constexpr int PER = kChunk / V / kThreads, BATCH = 8;
+    static_assert(PER * V * kThreads == kChunk && PER % BATCH == 0, "chunk / block mismatch");
 #pragma unroll
-    for (int j = 0; j < V; ++j) {
-      const double x = to_f(v[j]);
+    for (int k0 = 0; k0 < PER; k0 += BATCH) {
+      vec_t v[BATCH];
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k)
+        v[k] = reinterpret_cast<const vec_t *>(w)[threadIdx.x + (k0 + k) * kThreads];
+#pragma unroll
+      for (int k = 0; k < BATCH; ++k)
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const double x = to_f(v[k][j]);
+          acc += x * x;
+        }
+    }
+  } else {
+    const int nvec = ch.len / V;
+    for (int i = threadIdx.x; i < nvec; i += kThreads) {
+      const vec_t v = reinterpret_cast<const vec_t *>(w)[i];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const double x = to_f(v[j]);
+        acc += x * x;
+      }
+    }
+    for (int i = nvec * V + threadIdx.x; i < ch.len; i += kThreads) {
+      const double x = to_f(w[i]);
       acc += x * x;
     }
-  }
-  for (int i = nvec * V + threadIdx.x; i < ch.len; i += kThreads) {
-    const double x = to_f(w[i]);
-    acc += x * x;
   }
   const double r = block_sum<kThreads>(acc, sh);
   if (threadIdx.x == 0) part[blockIdx.x] = r;
@@ -241,9 +261,6 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
 
 // ---------------------------------------------------------------- finalize
 
-// Values and gradient factors; one wave per matrix reduces its trace
-// partials (lane-strided, fixed butterfly). One block; the set sum is taken
-// by thread 0 in index order.
 // Values and gradient factors: one 64-thread block per matrix, all matrices
 // at once. The trace partials of the matrix are summed by the wave (fixed
 // butterfly order).

@@ -14,7 +14,7 @@ namespace slorr {
 constexpr int kTile = 128;       // padding granularity = the small GEMM block tile
 constexpr int kBigTile = 256;    // the large GEMM block tile
 constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
-constexpr int kChunk = 8192;     // elements per block in the norm and gradient kernels
+constexpr int kChunk = 32768;    // elements per block in the norm and decoupled-update kernels
 constexpr int kThreads = 256;    // threads per block of the non-GEMM kernels
 constexpr int kXcds = 8;         // XCDs of an MI355X; workgroup b runs on XCD b % 8
 constexpr int kRedStripes = 4;   // split-K Gram reduce: blocks (row stripes) per tile
