@@ -98,6 +98,28 @@ def test_split_k_gram_long_rows(dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_nan_and_inf_stay_in_their_matrix(dtype):
+    """A NaN or Inf in one matrix reaches that matrix's value and gradient
+    and the set sum, and nothing else: the other matrices match the oracle."""
+    from workloads import f32_to_bf16_bits
+    shapes = [(64, 96), (130, 70), (96, 64), (70, 130)]
+    arrs = [gaussian(s, seed=77, std=0.05, dtype="f32", index=i) for i, s in enumerate(shapes)]
+    arrs[1] = arrs[1].copy()
+    arrs[1][5, 7] = np.nan
+    arrs[3] = arrs[3].copy()
+    arrs[3][0, 0] = np.inf
+    if dtype == "bf16":
+        arrs = [f32_to_bf16_bits(a) for a in arrs]
+    vals, grads, _ = run_gpu(arrs, dtype, "hoyer", 6)
+    assert not np.isfinite(vals[1]) and not np.isfinite(vals[3]) and not np.isfinite(vals[4])
+    assert not np.all(np.isfinite(grads[1])) and not np.all(np.isfinite(grads[3]))
+    clean = [0, 2]
+    refs = run_oracle([arrs[i] for i in clean], dtype, "hoyer", 6)
+    compare(np.array([vals[i] for i in clean] + [0.0]), [grads[i] for i in clean], refs, "hoyer", dtype,
+            label=f"nan/inf isolation {dtype}", check_total=False)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_empty_and_zero_matrices(dtype):
     import torch
     from paper_2607_08754_amd import Plan
