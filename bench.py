@@ -52,6 +52,47 @@ def _alg_bytes_per_launch(shapes, dtype, op):
     return float(tot)
 
 
+def integration_timings(cfg, kind, W, G, steps):
+    """The training-loop routes on the same set (one GPU): the autograd route
+    (forward with the gradient deferred, then the gradient kernel with the
+    upstream factors read on the device), the accumulate route (App. E.3,
+    one call with grad += lambda G) and the decoupled update kernel
+    (App. E.2, W <- W - s G_pre, timed on a copy of the weights)."""
+    import torch
+    from paper_2607_08754_amd import Plan
+    dev = W[0].device
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = ev(), ev()
+        a.record()
+        for _ in range(steps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / steps
+
+    out = {}
+    pd = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, defer_grad=True, device=dev)
+    scales = torch.full((cfg.n,), 0.5, dtype=torch.float32, device=dev)
+    fwd = timed(lambda: pd(W))
+    out["autograd_route_ms"] = round(timed(lambda: (pd(W), pd.grad(W, G, scales=scales))), 5)
+    out["autograd_forward_ms"] = round(fwd, 5)
+    pd.close()
+    pa = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, accumulate=True, device=dev)
+    out["accumulate_route_ms"] = round(timed(lambda: pa(W, G, grad_scale=1e-3)), 5)
+    Wc = [w.clone() for w in W]
+    apply_ms = timed(lambda: pa.apply_update(Wc, G, step=1e-6))
+    nbytes = sum(w.numel() * (2 * w.element_size() + 4) for w in W)   # read W and G, write W
+    out["decoupled_apply"] = {"avg_ms": round(apply_ms, 5), "alg_bytes": nbytes,
+                              "GB/s": round(nbytes / (apply_ms * 1e-3) / 1e9, 1)}
+    pa.close()
+    return out
+
+
 def _kernels_hash():
     """Hash of the library's sources (kernels and the plan that orders their tiles)."""
     csrc = os.path.join(ROOT, "paper_2607_08754_amd", "csrc")
@@ -283,6 +324,7 @@ def main():
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,
+        "integration": integration_timings(cfg, args.kind, W, G, 10),
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
