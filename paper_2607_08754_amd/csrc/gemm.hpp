@@ -345,9 +345,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 
   // ------------------------------------------------------------ epilogue
   // acc[i][j][r] holds row 8 (r / 4) + 4 lk + r % 4 and column lr of MFMA tile
-  // (i, j). Per 32-row block of the wave tile: stage in LDS (fp32), then
-  // finish row-wise with 16-byte accesses, then (mirror tiles, tall P) write
-  // the transpose column-wise.
+  // (i, j). Per 32-row block of the wave tile: stage in the wave's own LDS
+  // area (fp32), then finish row-wise with 16-byte accesses, then (mirror
+  // tiles, tall P) write the transpose column-wise. The waves do not wait for
+  // each other during the epilogue.
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
@@ -411,7 +412,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) ep[(8 * (r >> 2) + 4 * lk + (r & 3)) * P + j * 32 + lr] = acc[i][j][r];
-    __syncthreads();
+    // the staging area is the wave's own and one wave's LDS operations are
+    // performed in order: a wave-level barrier (no reordering) suffices
+    __builtin_amdgcn_wave_barrier();
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
 #pragma unroll
     for (int t = 0; t < NTASK; ++t) {
@@ -470,7 +473,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         e[1] = e1;
       }
     }
-    __syncthreads();
+    __builtin_amdgcn_wave_barrier();
     if (colwise) {
       // transpose: output row = this tile's column, 8 consecutive source rows
 #pragma unroll
@@ -489,10 +492,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
           tsum += wdot(i, i & 1, t, v);       // tall W (colwise only for tall)
         }
       }
-      __syncthreads();
+      __builtin_amdgcn_wave_barrier();
     }
   }
   if (MODE == kLast) {
+    __syncthreads();                      // the block sum reuses wave 0's staging area
     const double r = block_sum<NT>(tsum, reinterpret_cast<double *>(smem));
     if (tid == 0) args.tpart[tile.slot] = r;
   }
