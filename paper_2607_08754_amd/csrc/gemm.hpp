@@ -208,6 +208,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   if (tile.mat < 0) return;      // padding of the XCD-ordered list (whole block)
   // a Gram part (split K) covers k in [k0, k1) and stores its raw fp32 partial
   const bool part = MODE == kGram && tile.k1 > 0;
+  // diagonal Gram / poly tile (BM == BN): the A and B operands are the same
+  // row panel, loaded once and read for both
+  const bool diag = (MODE == kGram || MODE == kPoly) && BM == BN && tile.tm == tile.tn;
   const MatDesc d = args.mats[tile.mat];
   const int m0 = tile.tm * BM, n0 = tile.tn * BN;
   T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
@@ -251,6 +254,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       load_lds16(Ap + size_t(m0 + row) * lda + k0 + (pch ^ swz_key(row)) * V, sA + r0 * 128);
     }
     if constexpr (!KN) {
+      if (diag) return;                 // both operands are the same rows: one copy
 #pragma unroll
       for (int i = 0; i < BN / 8 / S::kWaves; ++i) {
         const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
@@ -303,7 +307,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s run
   auto compute = [&](int buf) {
     const char *sA = smem + buf * S::kStage;
-    const char *sB = sA + BM * 128;
+    const char *sB = diag ? sA : sA + BM * 128;
     frag fa[2][FM], fb[2][FN];
     auto read = [&](int s, int slot) {
 #pragma unroll
