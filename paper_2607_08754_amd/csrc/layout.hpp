@@ -17,6 +17,7 @@ constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
 constexpr int kChunk = 32768;    // elements per block in the norm and decoupled-update kernels
 constexpr int kThreads = 256;    // threads per block of the non-GEMM kernels
 constexpr int kXcds = 8;         // XCDs of an MI355X; workgroup b runs on XCD b % 8
+constexpr int kCus = 256;        // compute units of an MI355X
 constexpr int kRedStripes = 4;   // split-K Gram reduce: blocks (row stripes) per tile
 
 // Power-of-two operand scales of the fp16 iterate (bf16 weights). With the

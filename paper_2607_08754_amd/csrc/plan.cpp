@@ -15,8 +15,8 @@ namespace {
 constexpr int64_t kMaxShort = 16384;
 constexpr int64_t kMaxLong = 1 << 20;
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
-constexpr int64_t kMinBigTiles = 2 * 256;   // two 256-tiles per CU (256 CUs)
-constexpr int64_t kMinGramUnits = 2 * 256;  // Gram blocks wanted per launch (two per CU)
+constexpr int64_t kMinBigTiles = 2 * kCus;  // two 256-tiles per CU
+constexpr int64_t kMinGramUnits = 2 * kCus; // Gram blocks wanted per launch (two per CU)
 constexpr int kMaxGramParts = 16;           // k parts per Gram tile at most
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
