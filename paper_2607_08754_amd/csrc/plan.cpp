@@ -19,6 +19,15 @@ constexpr int64_t kMinBigTiles = 2 * kCus;  // two 256-tiles per CU
 constexpr int64_t kMinGramUnits = 2 * kCus; // Gram blocks wanted per launch (two per CU)
 constexpr int kMaxGramParts = 16;           // k parts per Gram tile at most
 
+Tile make_tile(int32_t mat, int32_t tm, int32_t tn, int32_t slot) {
+  Tile t{};
+  t.mat = mat;
+  t.tm = tm;
+  t.tn = tn;
+  t.slot = slot;
+  return t;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
 
@@ -151,7 +160,7 @@ void build_plan(Plan &p) {
     }
     for (size_t i = 0; i < longest; ++i)
       for (int x = 0; x < kXcds; ++x)
-        p.tiles.push_back(i < seq[x].size() ? seq[x][i] : Tile{-1, 0, 0, 0});
+        p.tiles.push_back(i < seq[x].size() ? seq[x][i] : make_tile(-1, 0, 0, 0));
     r.count = int32_t(p.tiles.size()) - r.first;
     return r;
   };
@@ -165,7 +174,7 @@ void build_plan(Plan &p) {
       Job j{i, double(d.Qp) + d.Pp, {}};
       const int nt = d.Pp / tsize(cfg);
       for (int tm = 0; tm < nt; ++tm)
-        for (int tn = tm; tn < nt; ++tn) j.tiles.push_back({i, tm, tn, 0});
+        for (int tn = tm; tn < nt; ++tn) j.tiles.push_back(make_tile(i, tm, tn, 0));
       jobs.push_back(std::move(j));
     }
     p.pp[cfg] = emit(std::move(jobs));
@@ -195,11 +204,11 @@ void build_plan(Plan &p) {
         const int nt = d.Pp / kTile;
         for (int tm = 0; tm < nt; ++tm)
           for (int tn = tm; tn < nt; ++tn) {
-            Tile r{i, tm, tn, p.gram_parts};
+            Tile r = make_tile(i, tm, tn, p.gram_parts);
             r.parts = parts;
             reds.push_back(r);
             for (int q = 0; q < parts; ++q) {
-              Tile t{i, tm, tn, p.gram_parts++};
+              Tile t = make_tile(i, tm, tn, p.gram_parts++);
               t.k0 = q * per * kTile;
               t.k1 = std::min(nblk, (q + 1) * per) * kTile;
               j.tiles.push_back(t);
@@ -223,7 +232,7 @@ void build_plan(Plan &p) {
       Job j{i, double(d.Pp), {}};
       d.trace_begin = slot;
       for (int tm = 0; tm < d.Pp / tsize(cfg); ++tm)
-        for (int tn = 0; tn < d.Qp / tsize(cfg); ++tn) j.tiles.push_back({i, tm, tn, slot++});
+        for (int tn = 0; tn < d.Qp / tsize(cfg); ++tn) j.tiles.push_back(make_tile(i, tm, tn, slot++));
       d.trace_end = slot;
       jobs.push_back(std::move(j));
     }
@@ -236,7 +245,7 @@ void build_plan(Plan &p) {
     MatDesc &d = p.mats[i];
     if (d.empty) continue;
     for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
-      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back({i, tm, tn, 0});
+      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, 0));
     const int64_t total = int64_t(d.rows) * d.cols;
     d.chunk_begin = int32_t(p.chunks.size());
     for (int64_t b = 0; b < total; b += kChunk)
