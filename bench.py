@@ -166,6 +166,7 @@ SWEEPS = {
     "vit": ["vit_ti", "vit_256", "vit_s", "vit_512", "vit_b16", "vit_b24", "vit_960_24", "vit_l16",
             "vit_1152_28", "vit_h"],
     "llm": ["llm135_paper", "llm560_paper", "llm560"],
+    "configs": ["tiny", "resnet18", "vit_b16", "vit_l16", "llm560"],
 }
 
 
@@ -225,9 +226,10 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
-    ap.add_argument("--sweep", choices=["vit", "llm", "all"], default=None,
-                    help="time every set of a scaling sweep (App. D ViT configurations, App. F LLM "
-                         "shapes) instead of the headline workload; prints one JSON line")
+    ap.add_argument("--sweep", choices=["vit", "llm", "configs", "all"], default=None,
+                    help="time every set of a sweep (App. D ViT configurations, App. F LLM shapes, "
+                         "or the five configured sets) instead of the headline workload; prints one "
+                         "JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the hot path has no "
