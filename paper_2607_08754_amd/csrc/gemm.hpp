@@ -151,6 +151,23 @@ template <> struct WChunk<float> {
   __device__ __forceinline__ float get(int j) const { return j < 4 ? a[j] : b[j - 4]; }
 };
 
+// 8 consecutive iterate values (fp16 or fp32) as loaded, for a load issued
+// ahead of its use.
+template <typename T> struct XChunk;
+template <> struct XChunk<_Float16> {
+  half8 h;
+  __device__ __forceinline__ void load(const _Float16 *p) { h = *reinterpret_cast<const half8 *>(p); }
+  __device__ __forceinline__ float get(int j) const { return float(h[j]); }
+};
+template <> struct XChunk<float> {
+  float4v a, b;
+  __device__ __forceinline__ void load(const float *p) {
+    a = reinterpret_cast<const float4v *>(p)[0];
+    b = reinterpret_cast<const float4v *>(p)[1];
+  }
+  __device__ __forceinline__ float get(int j) const { return j < 4 ? a[j] : b[j - 4]; }
+};
+
 // 8 consecutive values of type T from global memory (16-byte aligned).
 template <typename T>
 __device__ __forceinline__ void load8(const T *p, float (&v)[8]) {
@@ -407,11 +424,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     return s;
   };
   if constexpr (MODE == kLast) wprefetch(0, 0);
+  // Poly: the A values of the b A term, likewise one 32-row block ahead
+  XChunk<T> apre[2][NTASK];
+  auto aprefetch = [&](int i, int b) {
+    const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
+#pragma unroll
+    for (int t = 0; t < NTASK; ++t) {
+      const int task = lane + 64 * t;
+      apre[b][t].load(Am + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
+    }
+  };
+  if constexpr (MODE == kPoly) aprefetch(0, 0);
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if constexpr (MODE == kLast)
       if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
+    if constexpr (MODE == kPoly)
+      if (i + 1 < FM) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -444,10 +474,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
           store8(Am + size_t(grow) * d.Pp + gcol, v);
         }
       } else if (MODE == kPoly) {
-        float in[8];
-        load8(Am + size_t(grow) * d.Pp + gcol, in);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
+        for (int j = 0; j < 8; ++j)
+          v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
         store8(Bm + size_t(grow) * d.Pp + gcol, v);
       } else {
         if (args.fold) {
