@@ -223,6 +223,8 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-integration", action="store_true",
+                    help="skip the timings of the training-loop routes (keeps profiles to the hot path)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -326,7 +328,7 @@ def main():
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,
-        "integration": integration_timings(cfg, args.kind, W, G, 10),
+        "integration": None if args.no_integration else integration_timings(cfg, args.kind, W, G, 10),
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
