@@ -6,8 +6,11 @@
 //   Poly    B  = b A + c A A^T + a I   NT on the symmetric A (A A^T = A A); the
 //                                      a X term of the step is folded into B
 //   Update  X' = B X                   B symmetric (rows of B = columns of B);
-//                                      X is read as [k][n] and transposed into
-//                                      the K-major LDS layout on the way in.
+//                                      X is read as [k][n]: fp16 stages keep
+//                                      that layout in LDS and transpose on the
+//                                      LDS read (ds_read_b64_tr_b16); fp32 is
+//                                      transposed into the K-major layout on
+//                                      the way in.
 //                                      Cubic steps (no Poly) use X' = a X + b A X
 //                                      with the a X term in the epilogue.
 //   Last    X_T = B X, stored like an update, with the per-tile partial
@@ -24,10 +27,10 @@
 // stores of the NK loader (8 lanes per row) and of the transposing KN loader
 // (16 lanes per row, 8-byte pieces) are conflict-free too.
 //
-// Pipeline: two LDS stages, one barrier per k-slab. The K-major operands go
-// global -> LDS directly (no registers); the [k][n] operand of the update is
-// loaded into registers and stored transposed. The loads of slab k + 1 are in
-// flight while the MFMAs of slab k run.
+// Pipeline: two LDS stages, one barrier per k-slab. The K-major operands and
+// the fp16 [k][n] operand go global -> LDS directly (no registers); the fp32
+// [k][n] operand is loaded into registers and stored transposed. The loads of
+// slab k + 1 are in flight while the MFMAs of slab k run.
 // Included inside namespace slorr, after the helpers of kernels.hip.
 #pragma once
 
@@ -94,13 +97,53 @@ __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((ch
 // 16 bytes per lane from global memory straight into LDS: lane l's bytes land
 // at lds_base + 16 l (lds_base wave-uniform, passed in m0). Device pass only:
 // the host pass of the single-source build just needs the kernel's stub.
+//
+// Issued through inline assembly: the compiler then does not track these LDS
+// writes and puts no wait for them before later LDS reads (it cannot tell
+// that those read the other stage). Completion is the caller's job: the
+// block barrier at the end of each k-slab waits for every outstanding load.
 __device__ __forceinline__ void load_lds16(const void *g, void *lds_base) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  typedef __attribute__((address_space(3))) void lds_void;
-  __builtin_amdgcn_global_load_lds(g, (lds_void *)lds_base, 16, 0, 0);
+  // the low 32 bits of a flat address into LDS are the LDS byte address
+  const uint32_t m = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(lds_base)));
+  asm volatile("global_load_lds_dwordx4 %1, off" : : "{m0}"(m), "v"(g) : "memory");
 #else
   (void)g;
   (void)lds_base;
+#endif
+}
+
+// Transposing LDS read of 16-bit values (ds_read_b64_tr_b16). Within each
+// group of 16 lanes, lane s gives the address of 4 consecutive values: row
+// s / 4, columns 4 (s % 4) .. 4 (s % 4) + 3 of a 4 x 16 block; lane j then
+// holds column j of the block, element i from row i.
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ half4 lds_read_tr16(const void *lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((__vector_size__(4 * sizeof(__fp16)))) __fp16 fp16x4;
+  typedef __attribute__((address_space(3))) fp16x4 lds_fp16x4;
+  const fp16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_fp16x4 *)(lds));
+  return __builtin_bit_cast(half4, v);
+#else
+  (void)lds;
+  return half4{};
+#endif
+}
+
+// Byte offset of 16-byte chunk `chunk` of k-row `row`
+// of a [k][n] operand stage (rows of `pitch` bytes). The key 4 (row & 3)
+// spreads the 4 rows x 4 chunks that one half-wave reads with a transposing
+// read (rows r..r+3 of a 16-row step, 64 bytes each) over all 64 banks.
+__device__ __forceinline__ int kn_off(int row, int chunk, int pitch) {
+  return row * pitch + ((chunk ^ ((row & 3) << 2)) << 4);
+}
+
+// Wait until every global -> LDS load this wave issued has landed (the
+// compiler does not count them, see load_lds16); precedes the block barrier
+// that publishes a stage.
+__device__ __forceinline__ void lds_dma_wait() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
 #endif
 }
 
@@ -213,6 +256,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int BK = 8 * V;                      // k per slab (128-byte rows)
   constexpr int FM = S::FM, FN = S::FN, WTM = S::WTM, WTN = S::WTN;
   constexpr bool KN = (MODE == kUpdate || MODE == kLast);
+  // fp16 [k][n] operand: global -> LDS directly in its own layout, transposed
+  // on the LDS read; fp32 goes through registers and is stored transposed
+  constexpr bool TR = KN && sizeof(T) == 2;
+  constexpr int KNP = BN * int(sizeof(T));       // bytes per k-row of a [k][n] stage
   constexpr int QB = (BK / 4) * (BN / V) / NT;   // 4 x V blocks per thread, B slab (KN)
   static_assert(BM % (8 * S::kWaves) == 0 && BN % (8 * S::kWaves) == 0, "tile / wave mismatch");
   static_assert(!KN || QB * NT == (BK / 4) * (BN / V), "KN loader mismatch");
@@ -270,6 +317,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
       load_lds16(Ap + size_t(m0 + row) * lda + k0 + (pch ^ swz_key(row)) * V, sA + r0 * 128);
     }
+    if constexpr (TR) {
+      // one wave instruction fills 1024 / KNP consecutive k-rows; lane l lands
+      // at physical chunk l % (KNP / 16) of its row and fetches the logical
+      // chunk that kn_off puts there
+      constexpr int CPR = KNP / 16, RPI = 1024 / KNP;
+      const int rsub = lane / CPR, pch = lane % CPR;
+#pragma unroll
+      for (int i = 0; i < BK / RPI / S::kWaves; ++i) {
+        const int r0 = (wave + i * S::kWaves) * RPI, row = r0 + rsub;
+        load_lds16(Bp + size_t(k0 + row) * ldb + n0 + (pch ^ ((row & 3) << 2)) * V, sB + r0 * KNP);
+      }
+    }
     if constexpr (!KN) {
       if (diag) return;                 // both operands are the same rows: one copy
 #pragma unroll
@@ -280,9 +339,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     }
   };
   // the transposing loader of the [k][n] operand (update) into registers
-  frag rk[KN ? 4 * QB : 1];
+  frag rk[KN && !TR ? 4 * QB : 1];
   auto kload = [&](int k0) {
-    if constexpr (KN) {
+    if constexpr (KN && !TR) {
 #pragma unroll
       for (int i = 0; i < QB; ++i) {
         const int q = tid + i * NT, kq = q % (BK / 4), nc = q / (BK / 4);
@@ -293,7 +352,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     }
   };
   auto kstore = [&](int buf) {
-    if constexpr (KN) {
+    if constexpr (KN && !TR) {
       char *sB = smem + buf * S::kStage + BM * 128;
 #pragma unroll
       for (int i = 0; i < QB; ++i) {
@@ -331,8 +390,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       for (int i = 0; i < FM; ++i)
         fa[slot][i] = *reinterpret_cast<const frag *>(sA + swz(wm * WTM + i * 32 + lr, 2 * s + lk));
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        fb[slot][j] = *reinterpret_cast<const frag *>(sB + swz(wn * WTN + j * 32 + lr, 2 * s + lk));
+      for (int j = 0; j < FN; ++j) {
+        if constexpr (TR) {
+          // lane L: k = 16 s + 8 (L / 32) + 0..7 of column n = L % 32 of the
+          // fragment, as two transposing reads of 4 k-rows each
+          const int g = lane >> 4, si = lane & 15;
+          const int row = 16 * s + 8 * (g >> 1) + (si >> 2);
+          const int col = wn * WTN + j * 32 + 16 * (g & 1) + 4 * (si & 3);
+          const int off = kn_off(row, col >> 3, KNP) + 8 * (si & 1);
+          const half4 lo = lds_read_tr16(sB + off);
+          const half4 hi = lds_read_tr16(sB + off + 4 * KNP);
+          fb[slot][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        } else {
+          fb[slot][j] = *reinterpret_cast<const frag *>(sB + swz(wn * WTN + j * 32 + lr, 2 * s + lk));
+        }
+      }
     };
     read(0, 0);
 #pragma unroll
@@ -352,6 +424,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   dload(0, 0);
   kload(0);
   kstore(0);
+  lds_dma_wait();
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int nb = (kt + 1) & 1;
@@ -361,6 +434,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     }
     compute(kt & 1);
     if (kt + 1 < nk) kstore(nb);
+    lds_dma_wait();
     __syncthreads();
   }
 
