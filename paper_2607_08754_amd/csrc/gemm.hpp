@@ -229,6 +229,28 @@ __device__ __forceinline__ void load8(const T *p, float (&v)[8]) {
   }
 }
 
+// As store8, marked non-temporal: the iterate written by an update is read
+// only by the next launch, so its lines are not kept in this launch's L2,
+// where they would evict operand panels that other tiles still read.
+template <typename T>
+__device__ __forceinline__ void store8_stream(T *p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    half8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = _Float16(v[j]);
+    __builtin_nontemporal_store(h, reinterpret_cast<half8 *>(p));
+  } else {
+    float4v a, b;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      a[j] = v[j];
+      b[j] = v[4 + j];
+    }
+    __builtin_nontemporal_store(a, reinterpret_cast<float4v *>(p));
+    __builtin_nontemporal_store(b, reinterpret_cast<float4v *>(p) + 1);
+  }
+}
+
 template <typename T>
 __device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
   if constexpr (sizeof(T) == 2) {
@@ -562,7 +584,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
         }
-        if (MODE == kUpdate || args.write_x) store8(Xn + size_t(grow) * d.Qp + gcol, v);
+        if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale

@@ -108,6 +108,17 @@ void build_plan(Plan &p) {
   auto upd_cfg = [&](const MatDesc &d) {
     return (use_big && d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0) ? kCfg256 : kCfg128;
   };
+  // Gram: long k ranges (K = Qp), so the 256-tile's halved operand traffic
+  // pays as soon as the set has one upper-triangle 256-tile per CU. Poly
+  // (K = Pp, the shortest products) keeps the 128 tile: its 256-tiles would
+  // leave most CUs idle.
+  int64_t big_gram = 0;
+  for (int i : order) {
+    const MatDesc &d = p.mats[i];
+    if (d.Pp % kBigTile == 0) big_gram += int64_t(d.Pp / kBigTile) * (d.Pp / kBigTile + 1) / 2;
+  }
+  const bool gram_big = big_gram >= kCus;
+  auto gram_cfg = [&](const MatDesc &d) { return (gram_big && d.Pp % kBigTile == 0) ? kCfg256 : kCfg128; };
   auto pp_cfg = [](const MatDesc &) { return kCfg128; };
   auto tsize = [](int cfg) { return cfg == kCfg128 ? kTile : kBigTile; };
   p.tiles.clear();
@@ -166,19 +177,23 @@ void build_plan(Plan &p) {
   };
   // Gram and Poly outputs are symmetric: upper-triangle tiles only (the
   // kernel also stores the transpose of off-diagonal tiles)
-  for (int cfg = 0; cfg < kNumCfg; ++cfg) {
-    std::vector<Job> jobs;
-    for (int i : order) {
-      const MatDesc &d = p.mats[i];
-      if (pp_cfg(d) != cfg) continue;
-      Job j{i, double(d.Qp) + d.Pp, {}};
-      const int nt = d.Pp / tsize(cfg);
-      for (int tm = 0; tm < nt; ++tm)
-        for (int tn = tm; tn < nt; ++tn) j.tiles.push_back(make_tile(i, tm, tn, 0));
-      jobs.push_back(std::move(j));
+  auto sym_tiles = [&](auto cfg_of, TileRange *out, bool gram) {
+    for (int cfg = 0; cfg < kNumCfg; ++cfg) {
+      std::vector<Job> jobs;
+      for (int i : order) {
+        const MatDesc &d = p.mats[i];
+        if (cfg_of(d) != cfg) continue;
+        Job j{i, double(gram ? d.Qp : d.Pp), {}};
+        const int nt = d.Pp / tsize(cfg);
+        for (int tm = 0; tm < nt; ++tm)
+          for (int tn = tm; tn < nt; ++tn) j.tiles.push_back(make_tile(i, tm, tn, 0));
+        jobs.push_back(std::move(j));
+      }
+      out[cfg] = emit(std::move(jobs));
     }
-    p.pp[cfg] = emit(std::move(jobs));
-  }
+  };
+  sym_tiles(gram_cfg, p.gram, true);
+  sym_tiles(pp_cfg, p.pp, false);
   // Split-K Gram. A set with few Gram tiles (small P) but long K = Qp would
   // leave most CUs idle: every tile's k range is cut into parts (multiples of
   // kTile) so that the launch has about kMinGramUnits blocks; each part writes
@@ -189,14 +204,14 @@ void build_plan(Plan &p) {
   {
     int64_t ntiles = 0;
     for (int i : order)
-      if (pp_cfg(p.mats[i]) == kCfg128) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
+      if (gram_cfg(p.mats[i]) == kCfg128) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
     if (ntiles > 0 && ntiles < kMinGramUnits) {
       const int want = int(std::max<int64_t>(1, std::min<int64_t>(kMaxGramParts, kMinGramUnits / ntiles)));
       std::vector<Job> jobs;
       std::vector<Tile> reds;
       for (int i : order) {
         const MatDesc &d = p.mats[i];
-        if (pp_cfg(d) != kCfg128) continue;
+        if (gram_cfg(d) != kCfg128) continue;
         const int nblk = d.Qp / kTile;                     // k blocks of kTile
         const int per = (nblk + std::min(want, nblk) - 1) / std::min(want, nblk);
         const int parts = (nblk + per - 1) / per;
@@ -324,7 +339,7 @@ void build_plan(Plan &p) {
       l.alpha = galpha;
       p.launches.push_back(l);
     } else {
-      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg) gemm(Op::Gram, p.pp[cfg], cfg, wx, 0, 0, galpha, 0.0f, 0.0f);
+      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg) gemm(Op::Gram, p.gram[cfg], cfg, wx, 0, 0, galpha, 0.0f, 0.0f);
     }
     const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
     if (quintic) {

@@ -67,7 +67,8 @@ struct Plan {
   int32_t groups = 0;
   std::vector<MatDesc> mats;
   std::vector<Tile> tiles;             // all tile lists, concatenated
-  TileRange pp[kNumCfg];                     // P x P outputs (gram, poly), per GemmCfg
+  TileRange gram[kNumCfg];                   // P x P Gram outputs, per GemmCfg
+  TileRange pp[kNumCfg];                     // P x P poly outputs, per GemmCfg
   TileRange pq[kNumCfg];                     // P x Q outputs (update, last), per GemmCfg
   TileRange prep;                      // prep tiles over Pp x Qp
   TileRange gsplit, gred;              // split-K Gram: part entries, reduce entries

@@ -93,18 +93,23 @@ def test_plan_facts(L, name):
 
 def test_plan_symmetric_work_on_aligned_sets(L):
     """The headline sets are tile-aligned (no padding): per step the MFMAs run
-    Gram and Poly on upper-triangle 128 x 128 tiles and the full update."""
+    Gram on upper-triangle 256 x 256 tiles (these sets have at least one such
+    tile per CU), Poly on upper-triangle 128 x 128 tiles and the full update."""
     for name in ("vit_b16", "vit_l16", "llm560"):
         cfg = CONFIGS[name]
         st, h, _, _ = _plan(L, cfg.shapes, L.BF16, L.HOYER)
         info = L.PlanInfo()
         L.lib().slorr_plan_get_info(h, ctypes.byref(info))
         want = 0.0
+
+        def tri(P, t):
+            nt = P // t
+            return nt * (nt + 1) / 2 * float(t) * t
+
         for m, n in cfg.shapes:
             P, Q = min(m, n), max(m, n)
-            nt = P // 128
-            tri = nt * (nt + 1) / 2 * 128.0 * 128.0
-            want += cfg.iters * (2 * tri * Q + 2 * tri * P + 2.0 * P * P * Q)
+            assert P % 256 == 0
+            want += cfg.iters * (2 * tri(P, 256) * Q + 2 * tri(P, 128) * P + 2.0 * P * P * Q)
         assert info.mfma_flops == pytest.approx(want, rel=1e-12)
         L.lib().slorr_plan_destroy(h)
 
