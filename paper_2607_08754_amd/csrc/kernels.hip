@@ -391,7 +391,25 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   Tg *g = static_cast<Tg *>(dyn[t.mat].g);
   const float s1 = float(sc[t.mat].s1) * inv_sx, s2 = float(sc[t.mat].s2);
   const float gs = call->gscale ? call->grad_scale * call->gscale[t.mat] : call->grad_scale;
-  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+  // each thread has kTasks runs of 8 elements; W (and the old gradient) of
+  // its runs are loaded before X_T is staged, so that all of the block's
+  // reads are in flight together
+  constexpr int kTasks = kPrepTile * kPrepTile / 8 / kThreads;
+  const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;     // rows / columns of W
+  const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
+  float wv[kTasks][8], old[kTasks][8];
+#pragma unroll
+  for (int k = 0; k < kTasks; ++k) {
+    const int q = threadIdx.x + k * kThreads;
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+    const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
+    const size_t o = size_t(r0 + r) * d.cols + c0 + c;
+    get8(w + o, nv, wv[k]);
+    if (accumulate) get8(g + o, nv, old[k]);
+  }
+#pragma unroll
+  for (int k = 0; k < kTasks; ++k) {
+    const int q = threadIdx.x + k * kThreads;
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
     float v[8];
     get8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
@@ -399,27 +417,24 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
     for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j];
   }
   __syncthreads();
-  const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;     // rows / columns of W
-  const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
-  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+#pragma unroll
+  for (int k = 0; k < kTasks; ++k) {
+    const int q = threadIdx.x + k * kThreads;
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
     if (r0 + r >= rlim || c0 + c >= clim) continue;
     const int nv = min(8, clim - (c0 + c));
     const size_t o = size_t(r0 + r) * d.cols + c0 + c;
-    float wv[8], v[8];
-    get8(w + o, nv, wv);
+    float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float p = d.tall ? tile[(c + j) * kPrepPitch + r] : tile[r * kPrepPitch + c + j];
-      const float tj = s1 * p - s2 * wv[j];
+      const float tj = s1 * p - s2 * wv[k][j];
       v[j] = gs * tj;
       if constexpr (sizeof(Tg) == 2) v[j] = to_f(from_f<Tg>(v[j]));   // u rounded to bf16
     }
     if (accumulate) {
-      float old[8];
-      get8(g + o, nv, old);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = old[j] + v[j];
+      for (int j = 0; j < 8; ++j) v[j] = old[k][j] + v[j];
     }
     put8(g + o, nv, v);
   }
