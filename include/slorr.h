@@ -210,12 +210,13 @@ typedef enum {
   SLORR_OP_PREP = 2,      /* X_0 = W / (||W||_F + eps), short-side layout */
   SLORR_OP_GRAM = 3,      /* A = X X^T                                    */
   SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
-  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X                              */
+  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X; Gram space: M = B M_prev    */
   SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
   SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
-  SLORR_OP_GRAM_REDUCE = 10 /* sum of split-K Gram partials, A = X X^T     */
+  SLORR_OP_GRAM_REDUCE = 10, /* sum of split-K Gram partials, A = X X^T    */
+  SLORR_OP_SYM = 11       /* Gram space: C = B A                          */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the
@@ -245,6 +246,9 @@ typedef struct {
   double mfma_flops;       /* flops the MFMA units execute per call (padded tiles)   */
   double weight_bytes;     /* sum_i rows_i * cols_i * sizeof(dtype)                  */
   size_t workspace_bytes;
+  int32_t gram_space;      /* matrices iterated in Gram space (P x P products and    */
+                           /* X_T = M X_0; padded Q >= 2 P, quintic tables)          */
+  double m_scale;          /* scale of M in the iterate type                         */
 } slorr_plan_info_t;
 
 SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info);

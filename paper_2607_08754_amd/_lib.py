@@ -28,7 +28,8 @@ NO_GRAPH = 0x4
 AUX = 0x8
 DEFER_GRAD = 0x10
 
-OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce")
+OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce",
+       "sym")
 
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",
@@ -50,7 +51,8 @@ class PlanInfo(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("groups", ctypes.c_int32), ("iters", ctypes.c_int32),
                 ("launches", ctypes.c_int32), ("gemm_tiles", ctypes.c_int64),
                 ("paper_flops", ctypes.c_double), ("mfma_flops", ctypes.c_double),
-                ("weight_bytes", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t)]
+                ("weight_bytes", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t),
+                ("gram_space", ctypes.c_int32), ("m_scale", ctypes.c_double)]
 
 
 class SlorrError(RuntimeError):

@@ -264,13 +264,15 @@ slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
     int64_t tiles = 0;
     for (const auto &l : p.launches)
       if (l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Update ||
-          l.op == slorr::Op::Last)
+          l.op == slorr::Op::Last || l.op == slorr::Op::Sym)
         tiles += l.grid;
     info->gemm_tiles = tiles;
     info->paper_flops = p.paper_flops;
     info->mfma_flops = p.mfma_flops;
     info->weight_bytes = p.weight_bytes;
     info->workspace_bytes = p.ws_bytes;
+    info->gram_space = p.gs_count;
+    info->m_scale = p.m_scale;
     return SLORR_OK;
   });
 }

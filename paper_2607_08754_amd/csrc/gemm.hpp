@@ -67,9 +67,14 @@ struct GemmArgs {
   double *tpart;
   int which_x;    // current X buffer
   int use_a;      // update operand is A (cubic step)
+  int use_m;      // update operand is M (Gram space: X_T = M X_0)
+  int which_m;    // M buffer: written by a B M product, read by X_T = M X_0
+  int store_m;    // poly: also store M_0 = B, scaled by mscale, for Gram-space matrices
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
   float alpha, beta, gamma, inv_sx;
+  float alpha2;   // scale of the Gram-space products (A = B C, M = B M, C = B A)
+  float mscale;
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
 };
 
@@ -270,6 +275,18 @@ __device__ __forceinline__ void store8(T *p, const float (&v)[8]) {
   }
 }
 
+// Elements j in [lo, hi) of 8 consecutive values (one vector store when all 8).
+template <typename T>
+__device__ __forceinline__ void store8_range(T *p, const float (&v)[8], int lo, int hi) {
+  if (lo <= 0 && hi >= 8) {
+    store8(p, v);
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if (j >= lo && j < hi) p[j] = T(v[j]);
+}
+
 template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   using S = GemmShape<BM, BN, WGM, WGN>;
@@ -294,30 +311,41 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   if (tile.mat < 0) return;      // padding of the XCD-ordered list (whole block)
   // a Gram part (split K) covers k in [k0, k1) and stores its raw fp32 partial
   const bool part = MODE == kGram && tile.k1 > 0;
-  // diagonal Gram / poly tile (BM == BN): the A and B operands are the same
-  // row panel, loaded once and read for both
-  const bool diag = (MODE == kGram || MODE == kPoly) && BM == BN && tile.tm == tile.tn;
+  // diagonal tile of a product of a matrix with itself (X X^T, A A; BM == BN):
+  // the A and B operands are the same row panel, loaded once and read for both
+  const bool diag = (MODE == kGram || MODE == kPoly) && tile.op == 0 && BM == BN && tile.tm == tile.tn;
   const MatDesc d = args.mats[tile.mat];
   const int m0 = tile.tm * BM, n0 = tile.tn * BN;
   T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
   T *Xn = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x0 : d.x1));
   T *Am = reinterpret_cast<T *>(args.ws + d.a);
   T *Bm = reinterpret_cast<T *>(args.ws + d.b);
+  T *Cm = reinterpret_cast<T *>(args.ws + d.c);
+  T *Mw = reinterpret_cast<T *>(args.ws + (args.which_m ? d.m1 : d.m0));   // M written / read
+  T *Mr = reinterpret_cast<T *>(args.ws + (args.which_m ? d.m0 : d.m1));   // M_prev of B M
 
   const T *Ap;
   const T *Bp;
   int lda, ldb, K;
-  if (MODE == kGram) {
+  // the symmetric-output products, by tile.op (every operand but X is
+  // symmetric, so B Y = B Y^T is an NT product of rows)
+  if (MODE == kGram && tile.op == kOpXX) {          // A = X X^T
     Ap = Xc; Bp = Xc; lda = ldb = d.Qp; K = d.Qp;
     if (part) {
       Ap += tile.k0;
       Bp += tile.k0;
       K = tile.k1 - tile.k0;
     }
-  } else if (MODE == kPoly) {
-    Ap = Am; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
-  } else {
-    Ap = args.use_a ? Am : Bm; Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
+  } else if (MODE == kGram) {                        // A = B C (Gram space)
+    Ap = Bm; Bp = Cm; lda = ldb = d.Pp; K = d.Pp;
+  } else if (MODE == kPoly) {                        // A A, or B A (Gram space)
+    Ap = tile.op == kOpPoly ? Am : Bm;
+    Bp = Am;
+    lda = ldb = d.Pp; K = d.Pp;
+  } else if (tile.op == kOpBM) {                     // M = B M_prev (Gram space)
+    Ap = Bm; Bp = Mr; lda = ldb = d.Pp; K = d.Pp;
+  } else {                                           // B X, A X, or M X_0
+    Ap = args.use_m ? Mw : (args.use_a ? Am : Bm); Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
   }
 
   const int tid = threadIdx.x;
@@ -469,8 +497,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
-  const float alpha = args.alpha, beta = args.beta;
-  const bool mirror = (MODE == kGram || MODE == kPoly) && tile.tm != tile.tn && !part;
+  // Gram-space products scale by alpha2; the poly adds b A + a I
+  const bool gsp = (MODE == kGram || MODE == kPoly) && tile.op != 0;
+  const float alpha = gsp ? args.alpha2 : args.alpha, beta = args.beta;
+  // symmetric output and where it goes; the first poly of a Gram-space matrix
+  // also stores M_0 = B (scaled)
+  T *Sym = MODE == kGram ? Am : (tile.op == kOpPoly ? Bm : Cm);
+  const bool store_m0 = MODE == kPoly && tile.op == kOpPoly && args.store_m && d.gs;
+  // Symmetric outputs are stored exactly symmetric: off-diagonal tiles also
+  // store their transpose; a diagonal tile stores its upper triangle and the
+  // transpose of it below the diagonal (its own lower triangle, computed with
+  // a different rounding, is not used). The Gram-space products need this:
+  // with operands symmetric only up to rounding, B Y^T (the NT product) and
+  // B Y drift apart over the steps.
+  const bool mirror = (MODE == kGram || MODE == kPoly) && !part;
+  const bool dtile = mirror && tile.tm == tile.tn;
   const bool colwise = mirror || (MODE == kLast && d.tall);
   double tsum = 0.0;
   const Tw *W = (MODE == kLast) ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
@@ -530,14 +571,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       apre[b][t].load(Am + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
     }
   };
-  if constexpr (MODE == kPoly) aprefetch(0, 0);
+  if constexpr (MODE == kPoly)
+    if (!gsp) aprefetch(0, 0);
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if constexpr (MODE == kLast)
       if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
     if constexpr (MODE == kPoly)
-      if (i + 1 < FM) aprefetch(i + 1, (i + 1) & 1);
+      if (i + 1 < FM && !gsp) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -567,13 +609,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         } else {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= alpha;
-          store8(Am + size_t(grow) * d.Pp + gcol, v);
+          store8_range(Sym + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
         }
       } else if (MODE == kPoly) {
+        if (gsp) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
-        store8(Bm + size_t(grow) * d.Pp + gcol, v);
+          for (int j = 0; j < 8; ++j) v[j] *= alpha;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
+        }
+        const int lo = dtile ? grow - gcol : 0;
+        store8_range(Sym + size_t(grow) * d.Pp + gcol, v, lo, 8);
+        if (store_m0) {
+          float mv[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) mv[j] = v[j] * args.mscale;
+          store8_range(reinterpret_cast<T *>(args.ws + d.m0) + size_t(grow) * d.Pp + gcol, mv, lo, 8);
+        }
       } else {
         if (args.fold) {
 #pragma unroll
@@ -584,7 +638,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
         }
-        if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
+        if (MODE == kUpdate && tile.op == kOpBM) store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
+        else if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
@@ -613,10 +668,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = ep[(rg * 8 + j) * P + col];
         const int orow = gcol0 + col, ocol = grow0 + rg * 8;
-        if (MODE == kGram) {
-          store8(Am + size_t(orow) * d.Pp + ocol, v);
-        } else if (MODE == kPoly) {
-          store8(Bm + size_t(orow) * d.Pp + ocol, v);
+        if (MODE == kGram || MODE == kPoly) {
+          const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
+          store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
+          if (store_m0) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] *= args.mscale;
+            store8_range(reinterpret_cast<T *>(args.ws + d.m0) + size_t(orow) * d.Pp + ocol, v, 0, hi);
+          }
         } else if (MODE == kLast) {
           tsum += wdot(i, i & 1, t, v);       // tall W (colwise only for tall)
         }

@@ -317,9 +317,10 @@ __global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
 }
 
 // Split-K Gram: A tile = alpha * (sum of its fp32 partials, in part order),
-// stored with its transpose for off-diagonal tiles. kRedStripes blocks per
-// tile, each a stripe of rows; the stripe passes through LDS so that the
-// transposed store is row-contiguous too.
+// stored with its transpose for off-diagonal tiles; a diagonal tile stores
+// its upper triangle and the transpose of it below the diagonal (A exactly
+// symmetric). kRedStripes blocks per tile, each a stripe of rows; the stripe
+// passes through LDS so that the transposed store is row-contiguous too.
 template <typename Tx>
 __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict__ tiles,
                                                           const MatDesc *__restrict__ mats,
@@ -345,20 +346,37 @@ __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict
     for (int j = 0; j < 4; ++j) t[r][c + j] = alpha * acc[j];
   }
   __syncthreads();
+  const bool diag = e.tm == e.tn;
   for (int q = threadIdx.x; q < R * kTile / 8; q += kThreads) {
     const int r = (8 * q) / kTile, c = (8 * q) % kTile;
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = t[r][c + j];
-    put8(A + size_t(m0 + r) * d.Pp + n0 + c, 8, v);
-  }
-  if (e.tm != e.tn) {                 // the transpose: R consecutive columns per output row
-    for (int q = threadIdx.x; q < R * kTile / 8; q += kThreads) {
-      const int c = (8 * q) / R, r = (8 * q) % R;     // output row n0 + c, columns m0 + r ..
-      float v[8];
+    Tx *o = A + size_t(m0 + r) * d.Pp + n0 + c;
+    const int lo = diag ? (m0 + r) - (n0 + c) : 0;        // upper triangle of a diagonal tile
+    if (lo <= 0) {
+      put8(o, 8, v);
+    } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = t[r + j][c];
-      put8(A + size_t(n0 + c) * d.Pp + m0 + r, 8, v);
+      for (int j = 0; j < 8; ++j)
+        if (j >= lo) o[j] = from_f<Tx>(v[j]);
+    }
+  }
+  // the transpose: R consecutive columns per output row (strictly below the
+  // diagonal for a diagonal tile)
+  for (int q = threadIdx.x; q < R * kTile / 8; q += kThreads) {
+    const int c = (8 * q) / R, r = (8 * q) % R;     // output row n0 + c, columns m0 + r ..
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = t[r + j][c];
+    Tx *o = A + size_t(n0 + c) * d.Pp + m0 + r;
+    const int hi = diag ? (n0 + c) - (m0 + r) : 8;
+    if (hi >= 8) {
+      put8(o, 8, v);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j < hi) o[j] = from_f<Tx>(v[j]);
     }
   }
 }
@@ -378,7 +396,7 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
                                                    const DynDesc *__restrict__ dyn,
                                                    const Scalars *__restrict__ sc,
                                                    const CallParams *__restrict__ call,
-                                                   const char *__restrict__ ws, int xsel, float inv_sx,
+                                                   const char *__restrict__ ws, float inv_sx,
                                                    int accumulate) {
 #pragma clang fp contract(off)
   __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
@@ -386,7 +404,7 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   const MatDesc d = mats[t.mat];
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
   if (m0 >= d.P || n0 >= d.Q) return;                    // padding only (whole block)
-  const Tx *x = reinterpret_cast<const Tx *>(ws + (xsel ? d.x1 : d.x0));
+  const Tx *x = reinterpret_cast<const Tx *>(ws + d.xt);
   const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
   Tg *g = static_cast<Tg *>(dyn[t.mat].g);
   const float s1 = float(sc[t.mat].s1) * inv_sx, s2 = float(sc[t.mat].s2);
@@ -485,6 +503,7 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s) {
       hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
     case Op::Poly:
+    case Op::Sym:
       hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>), grid, block, 0, s, a);
       break;
     case Op::Update:
@@ -508,10 +527,10 @@ void launch_grad(const Plan &p, const Launch &l, hipStream_t s) {
   const int acc = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
   if (p.grad_dtype == SLORR_BF16)
     hipLaunchKernelGGL((k_grad<Tw, Tx, bf16_t>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
-                       call, ws, l.which_x, inv_sx, acc);
+                       call, ws, inv_sx, acc);
   else
     hipLaunchKernelGGL((k_grad<Tw, Tx, float>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
-                       call, ws, l.which_x, inv_sx, acc);
+                       call, ws, inv_sx, acc);
 }
 
 template <typename Tw, typename Tx>
@@ -543,6 +562,7 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         break;
       case Op::Gram:
       case Op::Poly:
+      case Op::Sym:
       case Op::Update:
       case Op::Last: {
         GemmArgs a;
@@ -553,10 +573,15 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.tpart = trace;
         a.which_x = l.which_x;
         a.use_a = l.use_a;
+        a.use_m = l.use_m;
+        a.which_m = l.which_m;
+        a.store_m = l.store_m;
         a.write_x = (p.flags & SLORR_VALUES_ONLY) ? 0 : 1;
         a.alpha = l.alpha;
         a.beta = l.beta;
         a.gamma = l.gamma;
+        a.alpha2 = l.alpha2;
+        a.mscale = l.mscale;
         a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);

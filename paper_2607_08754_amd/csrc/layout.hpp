@@ -37,7 +37,11 @@ struct MatDesc {
   int32_t empty;               // rows == 0 or cols == 0
   int32_t chunk_begin, chunk_end;   // slots in the norm-partials array
   int32_t trace_begin, trace_end;   // slots in the trace-partials array
+  int32_t gs;                  // iterated in Gram space (P x P products, X_T = M X_0)
+  int32_t pad;
   uint64_t x0, x1, a, b;            // byte offsets in the workspace
+  uint64_t c, m0, m1;               // Gram space: C = B A and the M ping-pong
+  uint64_t xt;                      // buffer holding X_T once the schedule has run
 };
 
 struct DynDesc {               // per call: caller pointers
@@ -55,8 +59,17 @@ struct CallParams {            // per call
 struct Tile {                  // one GEMM output tile / one prep tile / one Gram part
   int32_t mat, tm, tn, slot;   // mat < 0: padding entry, the block exits at once
   int32_t k0, k1;              // Gram part: its k range [k0, k1); k1 = 0: all of K
-  int32_t parts, pad;          // Gram reduce entry: partials slot .. slot + parts - 1
+  int32_t parts;               // Gram reduce entry: partials slot .. slot + parts - 1
+  int32_t op;                  // the tile's product (TileOp)
 };
+
+// Product of a GEMM tile. Gram launches (symmetric output): A = X X^T
+// (kOpXX) or, in Gram space, A = B C (kOpBC). Poly launches (symmetric
+// output): B = poly(A) (kOpPoly) or, in Gram space, C = B A (kOpBA). Update
+// launches (full output): X' = B X (kOpBX) or, in Gram space, M = B M_prev
+// (kOpBM), which is not symmetrised: B and M_prev commute only up to the
+// rounding of earlier steps.
+enum TileOp : int32_t { kOpXX = 0, kOpBC = 1, kOpPoly = 0, kOpBA = 1, kOpBX = 0, kOpBM = 1 };
 
 struct Chunk {                 // a contiguous run of a matrix's elements
   int32_t mat, begin, len, pad;

@@ -29,6 +29,47 @@ Tile make_tile(int32_t mat, int32_t tm, int32_t tn, int32_t slot) {
 }
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Gram-space iteration. With M_{-1} = I every iterate is X_t = M_t X_0,
+// M_t = B_t M_{t-1}, and (all B_t being polynomials of A_0 = X_0 X_0^T, so
+// that they commute) A_{t+1} = X_t X_t^T = B_t A_t B_t: the steps need only
+// P x P products (C = B A, A = B C, M = B M; all symmetric) and X_T = M X_0
+// once at the end: per step 8 P^3 instead of 4 P^2 Q + 2 P^3 flops.
+//
+// On a singular direction with normalised value x in [0, 1] (||X_0|| <= 1)
+// the matrices act as scalars: B_t = a + b y^2 + c y^4 at y = phi_{t-1}(x),
+// M_t = prod of the B's, C_t = B_t y^2. The table's worst values over a grid
+// of x bound the entries of the stored matrices (|entry| <= spectral norm).
+// For the fp16 iterate the scale of M is the largest power of two that keeps
+// |M| * s_m <= 2^14; the Gram space is refused (false) when M, B or C would
+// not fit the type or the table is not finite.
+bool gram_space_scale(const double *coeffs, int iters, bool f16, double *scale) {
+  double mmax = 0.0, bmax = 0.0, cmax = 0.0;
+  constexpr int kGrid = 4096;
+  for (int g = 0; g <= kGrid; ++g) {
+    double y = double(g) / kGrid, m = 1.0;
+    for (int t = 0; t < iters; ++t) {
+      const double a = coeffs[3 * t], b = coeffs[3 * t + 1], c = coeffs[3 * t + 2];
+      const double y2 = y * y, bt = a + b * y2 + c * y2 * y2;
+      m *= bt;
+      bmax = std::max(bmax, std::fabs(bt));
+      cmax = std::max(cmax, std::fabs(bt) * y2);
+      mmax = std::max(mmax, std::fabs(m));
+      y *= bt;
+    }
+  }
+  if (!std::isfinite(mmax) || !std::isfinite(bmax) || !std::isfinite(cmax) || mmax <= 0.0) return false;
+  if (!f16) {
+    *scale = 1.0;
+    return mmax < 1e30;
+  }
+  constexpr double kMax = 16384.0;
+  if (bmax * kScaleB16 > kMax || cmax * kScaleA16 > kMax) return false;
+  const double s = std::exp2(std::floor(std::log2(kMax / mmax)));
+  if (!(s >= 1.0 / 64.0)) return false;      // M would lose its small entries
+  *scale = std::min(s, 1024.0);
+  return true;
+}
 int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
 
 }  // namespace
@@ -60,13 +101,21 @@ void build_plan(Plan &p) {
 
   const bool f16 = p.dtype == SLORR_BF16;
   const float sx = f16 ? kScaleX16 : 1.0f, sa = f16 ? kScaleA16 : 1.0f, sb = f16 ? kScaleB16 : 1.0f;
-  bool any_quintic = false;
-  for (int t = 0; t < p.iters; ++t) any_quintic |= p.coeffs[3 * t + 2] != 0.0;
+  bool any_quintic = false, all_quintic = true;
+  for (int t = 0; t < p.iters; ++t) {
+    any_quintic |= p.coeffs[3 * t + 2] != 0.0;
+    all_quintic &= p.coeffs[3 * t + 2] != 0.0;
+  }
+  // Gram-space iteration, for matrices with Qp >= 2 Pp (see gram_space_scale)
+  double sm = 1.0;
+  const bool gs_ok = all_quintic && gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
+  p.m_scale = sm;
 
   // canonical shapes, groups
   p.mats.assign(p.n, MatDesc{});
   std::map<std::pair<int32_t, int32_t>, int> groups;
   p.paper_flops = p.mfma_flops = p.weight_bytes = 0;
+  p.gs_count = 0;
   for (int i = 0; i < p.n; ++i) {
     const int64_t r = p.shapes[i].rows, c = p.shapes[i].cols;
     if (r < 0 || c < 0) throw std::invalid_argument("negative matrix dimension");
@@ -84,42 +133,18 @@ void build_plan(Plan &p) {
     d.Qp = round_up(d.Q, kTile);
     if (r * c > kMaxElems || int64_t(d.Pp) * d.Qp > kMaxElems)
       throw std::domain_error("matrix has more than 2^31 - 1 elements");
+    d.gs = (gs_ok && d.Qp >= 2 * d.Pp) ? 1 : 0;
+    p.gs_count += d.gs;
     groups[{d.P, d.Q}]++;
     p.paper_flops += p.iters * (4.0 * P * P * Q + 2.0 * P * P * P);
     p.weight_bytes += double(r) * c * p.elem_bytes();
   }
   p.groups = int32_t(groups.size());
+  const int T = p.iters;
 
   std::vector<int> order;                 // non-empty matrices
   for (int i = 0; i < p.n; ++i)
     if (!p.mats[i].empty) order.push_back(i);
-  // Tile class of the P x Q products: the 256 x 256 block tile halves the
-  // operand traffic per flop of the 128 x 128 one but needs 256-aligned padded
-  // dims, and gives 4x fewer blocks: it is used only when the set's 256-tiles
-  // still fill the chip twice over (kMinBigTiles). The symmetric P x P
-  // products keep the 128 tile (half of their tiles are mirrored away).
-  int64_t big_tiles = 0;
-  for (int i : order) {
-    const MatDesc &d = p.mats[i];
-    if (d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0)
-      big_tiles += int64_t(d.Pp / kBigTile) * (d.Qp / kBigTile);
-  }
-  const bool use_big = big_tiles >= kMinBigTiles;
-  auto upd_cfg = [&](const MatDesc &d) {
-    return (use_big && d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0) ? kCfg256 : kCfg128;
-  };
-  // Gram: long k ranges (K = Qp), so the 256-tile's halved operand traffic
-  // pays as soon as the set has one upper-triangle 256-tile per CU. Poly
-  // (K = Pp, the shortest products) keeps the 128 tile: its 256-tiles would
-  // leave most CUs idle.
-  int64_t big_gram = 0;
-  for (int i : order) {
-    const MatDesc &d = p.mats[i];
-    if (d.Pp % kBigTile == 0) big_gram += int64_t(d.Pp / kBigTile) * (d.Pp / kBigTile + 1) / 2;
-  }
-  const bool gram_big = big_gram >= kCus;
-  auto gram_cfg = [&](const MatDesc &d) { return (gram_big && d.Pp % kBigTile == 0) ? kCfg256 : kCfg128; };
-  auto pp_cfg = [](const MatDesc &) { return kCfg128; };
   auto tsize = [](int cfg) { return cfg == kCfg128 ? kTile : kBigTile; };
   p.tiles.clear();
 
@@ -175,43 +200,78 @@ void build_plan(Plan &p) {
     r.count = int32_t(p.tiles.size()) - r.first;
     return r;
   };
-  // Gram and Poly outputs are symmetric: upper-triangle tiles only (the
-  // kernel also stores the transpose of off-diagonal tiles)
-  auto sym_tiles = [&](auto cfg_of, TileRange *out, bool gram) {
-    for (int cfg = 0; cfg < kNumCfg; ++cfg) {
-      std::vector<Job> jobs;
-      for (int i : order) {
-        const MatDesc &d = p.mats[i];
-        if (cfg_of(d) != cfg) continue;
-        Job j{i, double(gram ? d.Qp : d.Pp), {}};
-        const int nt = d.Pp / tsize(cfg);
-        for (int tm = 0; tm < nt; ++tm)
-          for (int tn = tm; tn < nt; ++tn) j.tiles.push_back(make_tile(i, tm, tn, 0));
-        jobs.push_back(std::move(j));
-      }
-      out[cfg] = emit(std::move(jobs));
-    }
+
+  // Symmetric-output products (Gram, poly, Gram-space products): upper-
+  // triangle tiles only; the kernel also stores the transpose of off-diagonal
+  // tiles. `prods` lists the products of one launch as (matrix, op, k extent);
+  // the 256-tile is used for every product of the launch when all of them
+  // allow it and the launch has at least `min_big` such tiles (it halves the
+  // operand traffic per flop of the 128-tile but gives 4x fewer blocks).
+  struct Prod {
+    int mat;
+    int32_t op;
+    int32_t k;
   };
-  sym_tiles(gram_cfg, p.gram, true);
-  sym_tiles(pp_cfg, p.pp, false);
+  auto sym_list = [&](const std::vector<Prod> &prods, int64_t min_big, TileRange *out) {
+    int64_t big = 0;
+    bool all_big = !prods.empty();
+    for (const Prod &q : prods) {
+      const int nb = p.mats[q.mat].Pp / kBigTile;
+      all_big &= p.mats[q.mat].Pp % kBigTile == 0;
+      big += int64_t(nb) * (nb + 1) / 2;
+    }
+    const int cfg = (all_big && big >= min_big) ? kCfg256 : kCfg128;
+    std::vector<Job> jobs;
+    for (const Prod &q : prods) {
+      Job j{q.mat, double(q.k), {}};
+      const int nt = p.mats[q.mat].Pp / tsize(cfg);
+      for (int tm = 0; tm < nt; ++tm)
+        for (int tn = tm; tn < nt; ++tn) {
+          Tile t = make_tile(q.mat, tm, tn, 0);
+          t.op = q.op;
+          j.tiles.push_back(t);
+        }
+      jobs.push_back(std::move(j));
+    }
+    for (int c = 0; c < kNumCfg; ++c) out[c] = TileRange{};
+    out[cfg] = emit(std::move(jobs));
+  };
+  // A_0 = X_0 X_0^T: long k ranges (K = Qp), so the 256-tile pays as soon as
+  // the set has one upper-triangle 256-tile per CU. The P x P products
+  // (K = Pp, the shortest) take it only with two per CU.
+  {
+    std::vector<Prod> g0, g1, pl, c0;
+    for (int i : order) {
+      const MatDesc &d = p.mats[i];
+      g0.push_back({i, kOpXX, d.Qp});
+      g1.push_back(d.gs ? Prod{i, kOpBC, d.Pp} : Prod{i, kOpXX, d.Qp});
+      pl.push_back({i, kOpPoly, d.Pp});
+      if (d.gs) c0.push_back({i, kOpBA, d.Pp});
+    }
+    sym_list(g0, kCus, p.gram);
+    if (p.gs_count && T > 1) sym_list(g1, kMinBigTiles, p.gram2);
+    else std::copy(p.gram, p.gram + kNumCfg, p.gram2);
+    sym_list(pl, kMinBigTiles, p.pp);
+    for (int c = 0; c < kNumCfg; ++c) p.sym_c[c] = TileRange{};
+    if (p.gs_count && T > 1) sym_list(c0, kMinBigTiles, p.sym_c);
+  }
   // Split-K Gram. A set with few Gram tiles (small P) but long K = Qp would
   // leave most CUs idle: every tile's k range is cut into parts (multiples of
   // kTile) so that the launch has about kMinGramUnits blocks; each part writes
-  // an fp32 partial tile, and a reduce launch adds the parts in order.
+  // an fp32 partial tile, and a reduce launch adds the parts in order. Used
+  // for X_0 X_0^T, and for every step when no matrix is in Gram space.
   p.gsplit = TileRange{};
   p.gred = TileRange{};
   p.gram_parts = 0;
-  {
+  if (p.gram[kCfg256].count == 0) {
     int64_t ntiles = 0;
-    for (int i : order)
-      if (gram_cfg(p.mats[i]) == kCfg128) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
+    for (int i : order) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
     if (ntiles > 0 && ntiles < kMinGramUnits) {
       const int want = int(std::max<int64_t>(1, std::min<int64_t>(kMaxGramParts, kMinGramUnits / ntiles)));
       std::vector<Job> jobs;
       std::vector<Tile> reds;
       for (int i : order) {
         const MatDesc &d = p.mats[i];
-        if (gram_cfg(d) != kCfg128) continue;
         const int nblk = d.Qp / kTile;                     // k blocks of kTile
         const int per = (nblk + std::min(want, nblk) - 1) / std::min(want, nblk);
         const int parts = (nblk + per - 1) / per;
@@ -237,21 +297,60 @@ void build_plan(Plan &p) {
       p.gred.count = int32_t(reds.size());
     }
   }
-  // Update tiles; each owns one trace-partial slot, contiguous per matrix
+  // Full-output products: the X-space updates (P x Q), in Gram space
+  // M = B M_prev (P x P) and X_T = M X_0 (P x Q). The tiles of the last
+  // product of a matrix (X-space update, X_T = M X_0) own one trace-partial
+  // slot each, contiguous per matrix. The 256-tile needs 256-aligned padded
+  // dims and is used when the launch's 256-tiles still fill the chip twice.
   int32_t slot = 0;
-  for (int cfg = 0; cfg < kNumCfg; ++cfg) {
+  struct Full {
+    int mat;
+    int32_t op;
+    int32_t n;            // output columns (Qp or Pp)
+  };
+  auto full_list = [&](const std::vector<Full> &prods, bool slots, TileRange *out) {
+    int64_t big = 0;
+    bool all_big = !prods.empty();
+    for (const Full &q : prods) {
+      const MatDesc &d = p.mats[q.mat];
+      all_big &= d.Pp % kBigTile == 0 && q.n % kBigTile == 0;
+      big += int64_t(d.Pp / kBigTile) * (q.n / kBigTile);
+    }
+    const int cfg = (all_big && big >= kMinBigTiles) ? kCfg256 : kCfg128;
     std::vector<Job> jobs;
-    for (int i : order) {
-      MatDesc &d = p.mats[i];
-      if (upd_cfg(d) != cfg) continue;
-      Job j{i, double(d.Pp), {}};
-      d.trace_begin = slot;
+    for (const Full &q : prods) {
+      MatDesc &d = p.mats[q.mat];
+      Job j{q.mat, double(d.Pp), {}};
+      if (slots) d.trace_begin = slot;
       for (int tm = 0; tm < d.Pp / tsize(cfg); ++tm)
-        for (int tn = 0; tn < d.Qp / tsize(cfg); ++tn) j.tiles.push_back(make_tile(i, tm, tn, slot++));
-      d.trace_end = slot;
+        for (int tn = 0; tn < q.n / tsize(cfg); ++tn) {
+          Tile t = make_tile(q.mat, tm, tn, slots ? slot++ : 0);
+          t.op = q.op;
+          j.tiles.push_back(t);
+        }
+      if (slots) d.trace_end = slot;
       jobs.push_back(std::move(j));
     }
-    p.pq[cfg] = emit(std::move(jobs));
+    for (int c = 0; c < kNumCfg; ++c) out[c] = TileRange{};
+    out[cfg] = emit(std::move(jobs));
+  };
+  {
+    std::vector<Full> xs, mix, ms, fs;
+    for (int i : order) {
+      const MatDesc &d = p.mats[i];
+      if (d.gs) {
+        mix.push_back({i, kOpBM, d.Pp});
+        ms.push_back({i, kOpBM, d.Pp});
+        fs.push_back({i, kOpBX, d.Qp});
+      } else {
+        xs.push_back({i, kOpBX, d.Qp});
+        mix.push_back({i, kOpBX, d.Qp});
+      }
+    }
+    full_list(xs, true, p.pq);
+    full_list(fs, true, p.fin);
+    full_list(ms, false, p.mprod);
+    full_list(mix, false, p.pqm);
   }
   p.trace_slots = slot;
   p.chunks.clear();
@@ -296,6 +395,15 @@ void build_plan(Plan &p) {
     d.x1 = take(pq);
     d.a = take(pp);
     d.b = any_quintic ? take(pp) : d.a;
+    if (d.gs) {
+      d.c = take(pp);
+      d.m0 = take(pp);
+      d.m1 = take(pp);
+      d.xt = d.x1;                            // X_T = M X_0 is written to x1
+    } else {
+      d.c = d.m0 = d.m1 = d.a;
+      d.xt = (T & 1) ? d.x1 : d.x0;           // step t reads x[t & 1], writes the other
+    }
   }
   p.ws_bytes = off;
 
@@ -311,58 +419,96 @@ void build_plan(Plan &p) {
   if (!p.chunks.empty()) p.launches.push_back(plain(Op::SumSq, int32_t(p.chunks.size())));
   if (p.n > 0) p.launches.push_back(plain(Op::NormFin, (p.n + kThreads / 64 - 1) / (kThreads / 64)));
   if (p.prep.count) p.launches.push_back(plain(Op::Prep, p.prep.count, p.prep.first));
-  auto gemm = [&](Op op, const TileRange &r, int cfg, int32_t wx, int32_t use_a, int32_t fold, float alpha,
-                  float beta, float gamma) {
-    if (!r.count) return;
-    Launch l{};
-    l.op = op;
-    l.grid = r.count;
-    l.tile_first = r.first;
-    l.cfg = cfg;
-    l.which_x = wx;
-    l.use_a = use_a;
-    l.fold = fold;
-    l.alpha = alpha;
-    l.beta = beta;
-    l.gamma = gamma;
-    p.launches.push_back(l);
+  auto gemm = [&](Op op, const TileRange *r, Launch l) {
+    for (int cfg = kNumCfg - 1; cfg >= 0; --cfg) {
+      if (!r[cfg].count) continue;
+      l.op = op;
+      l.grid = r[cfg].count;
+      l.tile_first = r[cfg].first;
+      l.cfg = cfg;
+      p.launches.push_back(l);
+    }
   };
-  for (int t = 0; t < p.iters; ++t) {
+  const float prod = float(1.0 / sb);           // (B_s Y_s) / s_b keeps Y's scale
+  for (int t = 0; t < T; ++t) {
     const double a = p.coeffs[3 * t], b = p.coeffs[3 * t + 1], c = p.coeffs[3 * t + 2];
     const int32_t wx = t & 1;
     const bool quintic = c != 0.0;
-    // A_s = s_a A  with  A = X X^T = (X_s X_s^T) / s_x^2
-    const float galpha = float(sa / (double(sx) * sx));
-    if (p.gsplit.count) {
-      gemm(Op::Gram, p.gsplit, kCfg128, wx, 0, 0, galpha, 0.0f, 0.0f);     // fp32 partials
+    // A: A_s = s_a A with A = X X^T = (X_s X_s^T) / s_x^2; in Gram space
+    // (later steps) A = B C of the previous step
+    Launch g{};
+    g.which_x = wx;
+    g.alpha = float(sa / (double(sx) * sx));
+    g.alpha2 = prod;
+    if (p.gsplit.count && (t == 0 || !p.gs_count)) {
+      g.op = Op::Gram;
+      g.grid = p.gsplit.count;
+      g.tile_first = p.gsplit.first;
+      g.cfg = kCfg128;
+      p.launches.push_back(g);                // fp32 partials
       Launch l = plain(Op::GramReduce, p.gred.count * kRedStripes, p.gred.first);
-      l.alpha = galpha;
+      l.alpha = g.alpha;
       p.launches.push_back(l);
     } else {
-      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg) gemm(Op::Gram, p.gram[cfg], cfg, wx, 0, 0, galpha, 0.0f, 0.0f);
+      gemm(Op::Gram, t == 0 ? p.gram : p.gram2, g);
     }
-    const Op op = (t == p.iters - 1) ? Op::Last : Op::Update;
+    const Op op = (t == T - 1) ? Op::Last : Op::Update;
     if (quintic) {
       // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
-      // the step X' = a X + (b A + c A A) X becomes X' = B X
-      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
-        gemm(Op::Poly, p.pp[cfg], cfg, wx, 0, 0, float(double(sb) * c / (double(sa) * sa)),
-             float(double(sb) * b / sa), float(double(sb) * a));
-      // X'_s = (B_s X_s) / s_b
-      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
-        gemm(op, p.pq[cfg], cfg, wx, 0, 1, float(1.0 / sb), 0.0f, 0.0f);
+      // the step X' = a X + (b A + c A A) X becomes X' = B X. The first poly
+      // also stores M_0 = B for the Gram-space matrices, at M's scale.
+      Launch l{};
+      l.which_x = wx;
+      l.alpha = float(double(sb) * c / (double(sa) * sa));
+      l.beta = float(double(sb) * b / sa);
+      l.gamma = float(double(sb) * a);
+      l.store_m = (t == 0 && p.gs_count) ? 1 : 0;
+      l.mscale = float(sm / sb);
+      gemm(Op::Poly, p.pp, l);
+      // X'_s = (B_s X_s) / s_b; Gram space (after the first step, where
+      // M_0 = B): M_t = B M_{t-1}, read from m[(t - 1) & 1], written to m[t & 1]
+      Launch u{};
+      u.which_x = wx;
+      u.which_m = t & 1;
+      u.fold = 1;
+      u.alpha = prod;
+      if (t == 0 || !p.gs_count) {
+        gemm(op, p.pq, u);
+      } else if (t < T - 1) {
+        gemm(Op::Update, p.pqm, u);
+      } else {
+        gemm(Op::Last, p.pq, u);
+        gemm(Op::Update, p.mprod, u);
+      }
+      // Gram space: C = B A for the next step's A = B C
+      Launch sp{};
+      sp.alpha2 = prod;
+      if (p.gs_count && t < T - 1) gemm(Op::Sym, p.sym_c, sp);
     } else {
-      // cubic step: X'_s = a X_s + b (A_s X_s) / s_a
-      for (int cfg = kNumCfg - 1; cfg >= 0; --cfg)
-        gemm(op, p.pq[cfg], cfg, wx, 1, 0, float(b / sa), float(a), 0.0f);
+      // cubic step (no Gram-space matrices): X'_s = a X_s + b (A_s X_s) / s_a
+      Launch u{};
+      u.which_x = wx;
+      u.use_a = 1;
+      u.alpha = float(b / sa);
+      u.beta = float(a);
+      gemm(op, p.pq, u);
     }
+  }
+  // Gram space: X_T = M_{T-1} X_0, with the trace partials
+  if (p.gs_count) {
+    Launch f{};
+    f.which_x = 0;
+    f.use_m = 1;
+    f.which_m = (T - 1) & 1;
+    f.fold = 1;
+    f.alpha = float(1.0 / sm);
+    gemm(Op::Last, p.fin, f);
   }
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
   p.launches.push_back(plain(Op::SetSum, 1));
   p.grad_launch = Launch{};
   if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {
     Launch l = plain(Op::Grad, p.prep.count, p.prep.first);
-    l.which_x = p.iters & 1;                  // buffer the last update wrote
     p.grad_launch = l;
     if (!(p.flags & SLORR_DEFER_GRAD)) p.launches.push_back(l);
   }
@@ -370,14 +516,15 @@ void build_plan(Plan &p) {
   // MFMA work the launches execute (padded, symmetric tiles counted once)
   p.mfma_flops = 0;
   for (const Launch &l : p.launches) {
-    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last) continue;
+    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last && l.op != Op::Sym)
+      continue;
     const double ts = tsize(l.cfg);
     for (int k = 0; k < l.grid; ++k) {
-      const int mi = p.tiles[l.tile_first + k].mat;
-      if (mi < 0) continue;
-      const MatDesc &d = p.mats[mi];
       const Tile &tl = p.tiles[l.tile_first + k];
-      const double kk = l.op == Op::Gram ? (tl.k1 > 0 ? double(tl.k1 - tl.k0) : double(d.Qp)) : double(d.Pp);
+      if (tl.mat < 0) continue;
+      const MatDesc &d = p.mats[tl.mat];
+      double kk = double(d.Pp);
+      if (l.op == Op::Gram && tl.op == kOpXX) kk = tl.k1 > 0 ? double(tl.k1 - tl.k0) : double(d.Qp);
       p.mfma_flops += 2.0 * ts * ts * kk;
     }
   }

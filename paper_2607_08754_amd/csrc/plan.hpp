@@ -26,7 +26,8 @@ enum class Op : int {
   Finalize = SLORR_OP_FINALIZE,  // values and gradient factors, one block per matrix
   Grad = SLORR_OP_GRAD,          // grad = g (s1 P - s2 W)   (original orientation)
   SetSum = SLORR_OP_SETSUM,      // set total in index order
-  GramReduce = SLORR_OP_GRAM_REDUCE  // A = sum of the split-K Gram partials
+  GramReduce = SLORR_OP_GRAM_REDUCE,  // A = sum of the split-K Gram partials
+  Sym = SLORR_OP_SYM             // Gram space: C = B A
 };
 
 // GEMM block-tile configurations (kernel template instances).
@@ -43,8 +44,13 @@ struct Launch {
   int32_t cfg;         // GemmCfg of a GEMM launch
   int32_t which_x;     // current X buffer (0: x0, 1: x1)
   int32_t use_a;       // update operand is A (cubic step) instead of B
+  int32_t use_m;       // update operand is M (Gram space: X_T = M X_0)
+  int32_t which_m;     // M buffer written (products) or read (X_T = M X_0)
+  int32_t store_m;     // poly: also store M_0 = B (Gram-space matrices)
   int32_t fold;        // update: a_t I already folded into B (no a X term)
   float alpha, beta, gamma;  // epilogue coefficients
+  float alpha2;        // Gram-space products (A = B C, M = B M, C = B A)
+  float mscale;        // poly: scale of the stored M_0 relative to B
 };
 
 struct TileRange {
@@ -67,9 +73,16 @@ struct Plan {
   int32_t groups = 0;
   std::vector<MatDesc> mats;
   std::vector<Tile> tiles;             // all tile lists, concatenated
-  TileRange gram[kNumCfg];                   // P x P Gram outputs, per GemmCfg
+  TileRange gram[kNumCfg];                   // A of the first step: X_0 X_0^T, every matrix
+  TileRange gram2[kNumCfg];                  // A of later steps: X X^T or (Gram space) B C
   TileRange pp[kNumCfg];                     // P x P poly outputs, per GemmCfg
-  TileRange pq[kNumCfg];                     // P x Q outputs (update, last), per GemmCfg
+  TileRange pq[kNumCfg];                     // P x Q outputs (update, last) of X-space matrices
+  TileRange pqm[kNumCfg];                    // X-space updates and Gram-space M = B M_prev
+  TileRange mprod[kNumCfg];                  // Gram space: M = B M_prev
+  TileRange fin[kNumCfg];                    // Gram space: X_T = M X_0
+  TileRange sym_c[kNumCfg];                  // Gram space: C = B A
+  int32_t gs_count = 0;                      // matrices iterated in Gram space
+  double m_scale = 1.0;                      // scale of M in the iterate type
   TileRange prep;                      // prep tiles over Pp x Qp
   TileRange gsplit, gred;              // split-K Gram: part entries, reduce entries
   int32_t gram_parts = 0;              // fp32 partial tiles in the workspace

@@ -4,6 +4,7 @@ agrees with the oracle's independent one, plans report the right facts, and
 every argument error is reported before anything touches a device.
 """
 import ctypes
+import math
 import os
 import re
 
@@ -63,6 +64,46 @@ def _plan(L, shapes, dtype=0, kind=0, opts=None):
     return st, h, ws.value, arr
 
 
+def _pad(x):
+    return (x + 127) // 128 * 128
+
+
+def _tri(P, t):
+    nt = P // t
+    return nt * (nt + 1) / 2 * float(t) * t
+
+
+def _expected_mfma(shapes, T):
+    """MFMA work of the schedule. Symmetric products (A, B, C) run on upper-
+    triangle tiles: 256 x 256 when every matrix of the launch is 256-aligned
+    and the launch has one such tile per CU for X_0 X_0^T, two per CU for the
+    other launches; full products (B X, M = B M_prev, X_T = M X_0) on all
+    tiles. Matrices with padded Q >= 2 P iterate in Gram space."""
+    mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
+    gs = [Q >= 2 * P for P, Q in mats]
+
+    def cfg(ps, min_big):
+        big = sum((P // 256) * (P // 256 + 1) // 2 for P in ps)
+        return 256 if ps and all(P % 256 == 0 for P in ps) and big >= min_big else 128
+
+    ps = [P for P, _ in mats]
+    gps = [P for (P, _), g in zip(mats, gs) if g]
+    t0 = cfg(ps, 256)
+    tot = sum(2 * _tri(P, t0) * Q for P, Q in mats)                      # A = X_0 X_0^T
+    if gps and T > 1:
+        t1 = cfg(ps, 512)
+        tot += (T - 1) * sum(2 * _tri(P, t1) * (P if g else Q) for (P, Q), g in zip(mats, gs))
+        tc = cfg(gps, 512)
+        tot += (T - 1) * sum(2 * _tri(P, tc) * P for P in gps)          # C = B A
+        tot += (T - 1) * sum(2.0 * P ** 3 for P in gps)                  # M = B M_prev
+    else:
+        tot += (T - 1) * sum(2 * _tri(P, t0) * Q for P, Q in mats)
+    tp = cfg(ps, 512)
+    tot += T * sum(2 * _tri(P, tp) * P for P, _ in mats)                 # poly
+    tot += sum(2.0 * P * P * Q * (1 if g else T) for (P, Q), g in zip(mats, gs))   # B X, M X_0
+    return tot, sum(gs)
+
+
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_plan_facts(L, name):
     cfg = CONFIGS[name]
@@ -76,42 +117,56 @@ def test_plan_facts(L, name):
     assert lib.slorr_plan_get_info(h, ctypes.byref(info)) == L.OK
     assert info.n == cfg.n and info.iters == cfg.iters
     assert info.paper_flops == pytest.approx(cfg.flops(), rel=1e-12)
-    # executed MFMA work: Gram and Poly over upper-triangle tiles only, on the
-    # zero-padded shapes; never below the symmetric minimum T (3 P^2 Q + P^3)
-    sym_min = cfg.iters * sum(3.0 * min(s) ** 2 * max(s) + min(s) ** 3 for s in cfg.shapes)
-    assert sym_min <= info.mfma_flops
+    want, ngs = _expected_mfma(cfg.shapes, cfg.iters)
+    assert info.gram_space == ngs
+    assert info.mfma_flops == pytest.approx(want, rel=1e-12)
     assert info.mfma_flops <= info.paper_flops * (1.0 if name in ("vit_b16", "vit_l16", "llm560") else 4.0)
     assert info.groups == len({(min(s), max(s)) for s in cfg.shapes})
-    # sumsq, norm, prep, 3 GEMM stages per step (one or two tile classes each),
-    # finalize, grad
-    assert 3 + 3 * cfg.iters + 3 <= info.launches <= 3 + 6 * cfg.iters + 3
+    # sumsq, norm, prep, the GEMM stages of each step (one or two tile classes
+    # each), X_T = M X_0, finalize, set sum, grad
+    assert 3 + 3 * cfg.iters + 3 <= info.launches <= 3 + 9 * cfg.iters + 5
     assert info.workspace_bytes == ws > 0
     esz = 2 if cfg.dtype == "bf16" else 4
     assert info.weight_bytes == sum(r * c * esz for r, c in cfg.shapes)
     assert lib.slorr_plan_destroy(h) == L.OK
 
 
-def test_plan_symmetric_work_on_aligned_sets(L):
-    """The headline sets are tile-aligned (no padding): per step the MFMAs run
-    Gram on upper-triangle 256 x 256 tiles (these sets have at least one such
-    tile per CU), Poly on upper-triangle 128 x 128 tiles and the full update."""
-    for name in ("vit_b16", "vit_l16", "llm560"):
-        cfg = CONFIGS[name]
-        st, h, _, _ = _plan(L, cfg.shapes, L.BF16, L.HOYER)
-        info = L.PlanInfo()
-        L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-        want = 0.0
-
-        def tri(P, t):
-            nt = P // t
-            return nt * (nt + 1) / 2 * float(t) * t
-
-        for m, n in cfg.shapes:
-            P, Q = min(m, n), max(m, n)
-            assert P % 256 == 0
-            want += cfg.iters * (2 * tri(P, 256) * Q + 2 * tri(P, 128) * P + 2.0 * P * P * Q)
-        assert info.mfma_flops == pytest.approx(want, rel=1e-12)
-        L.lib().slorr_plan_destroy(h)
+def test_plan_gram_space_selection(L):
+    """Gram space is taken for padded Q >= 2 P and quintic tables only; a cubic
+    table, or a table whose M would not fit the fp16 iterate, keeps every
+    matrix in X space."""
+    shapes = [(128, 256), (256, 128), (128, 255), (384, 640), (256, 256), (64, 576)]
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
+    assert st == L.OK
+    info = L.PlanInfo()
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 4          # 128 x 256 both ways, 128 x 255, 64 x 576 (padded 128 x 640)
+    # fp16 iterate: M's scale is a power of two with |M| s_m <= 2^14
+    assert info.m_scale > 0 and math.log2(info.m_scale) == int(math.log2(info.m_scale))
+    L.lib().slorr_plan_destroy(h)
+    opts = L.Options()
+    L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.degree = 3
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
+    assert st == L.OK
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 0
+    L.lib().slorr_plan_destroy(h)
+    # a table whose products grow beyond the fp16 range: a = 2^10 each step
+    tab = (ctypes.c_double * 9)(*([1024.0, 0.0, 1e-9] * 3))
+    L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.iters = 3
+    opts.coeffs = ctypes.cast(tab, ctypes.POINTER(ctypes.c_double))
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
+    assert st == L.OK
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 0
+    L.lib().slorr_plan_destroy(h)
+    # fp32: no range limit on M
+    st, h, _, _ = _plan(L, shapes, L.F32, L.HOYER, opts)
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 4 and info.m_scale == 1.0
+    L.lib().slorr_plan_destroy(h)
 
 
 def test_empty_plans(L):
@@ -300,9 +355,10 @@ def test_deferred_gradient_and_apply_checks_before_device_use(L):
 
 
 def test_split_k_gram_plan(L):
-    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch
-    per step; the parts cover every k exactly once (same executed MFMA work
-    as one pass per tile). Sets with enough tiles are not split."""
+    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch:
+    every step for X-space matrices, the first step (X_0 X_0^T) for Gram-space
+    ones; the parts cover every k exactly once (same executed MFMA work as one
+    pass per tile). Sets with enough tiles are not split."""
     def facts(shapes):
         st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
         assert st == L.OK
@@ -310,17 +366,18 @@ def test_split_k_gram_plan(L):
         L.lib().slorr_plan_get_info(h, ctypes.byref(info))
         L.lib().slorr_plan_destroy(h)
         return info
-    shapes = [(256, 4096), (4096, 256), (384, 2944)]           # 3 + 3 + 6 Gram tiles
-    info = facts(shapes)
     T = 6
+    xs = [(384, 640), (640, 384), (256, 384)]                # X space: padded Q < 2 P
+    info = facts(xs)
+    assert info.gram_space == 0
     assert info.launches == 3 + 4 * T + 3                    # gram parts, reduce, poly, update
-    want = 0.0
-    for m, n in shapes:
-        P, Q = min(m, n), max(m, n)
-        Pp, Qp = -(-P // 128) * 128, -(-Q // 128) * 128
-        nt = Pp // 128
-        tri = nt * (nt + 1) / 2 * 128.0 * 128.0
-        want += T * (2 * tri * Qp + 2 * tri * Pp + 2.0 * Pp * Pp * Qp)
-    assert info.mfma_flops == pytest.approx(want, rel=1e-12)
-    big = facts(CONFIGS["vit_b16"].shapes)
-    assert big.launches == 3 + 3 * 6 + 3
+    assert info.mfma_flops == pytest.approx(_expected_mfma(xs, T)[0], rel=1e-12)
+    gs = [(256, 4096), (4096, 256), (384, 2944)]             # Gram space, 3 + 3 + 6 Gram tiles
+    info = facts(gs)
+    assert info.gram_space == 3
+    # first step: gram parts, reduce, poly, C = B A; later steps: A = B C, poly,
+    # M = B M_prev, C = B A (not in the last step); then X_T = M X_0
+    assert info.launches == 3 + 4 + 4 * (T - 2) + 3 + 1 + 3
+    assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T)[0], rel=1e-12)
+    big = facts(CONFIGS["vit_b16"].shapes)                  # no split: A, poly, B X, B M / B A
+    assert big.launches == 3 + 4 * 6 + 1 + 3
