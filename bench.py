@@ -26,18 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA: fp16/bf16 operands, fp32 operands
-GEMM_OPS = ("gram", "poly", "update", "last")
-
-
-def _alg_flops_per_launch(shapes, op):
-    """Paper count (Sec. 3): per step 2 P^2 Q (A = X X^T) + 2 P^3 (A A) + 2 P^2 Q (B X)."""
-    tot = 0.0
-    for m, n in shapes:
-        if m == 0 or n == 0:
-            continue
-        P, Q = min(m, n), max(m, n)
-        tot += 2.0 * P ** 3 if op == "poly" else 2.0 * P * P * Q
-    return tot
+GEMM_OPS = ("gram", "poly", "update", "last", "sym")
 
 
 def _alg_bytes_per_launch(shapes, dtype, op):
@@ -200,10 +189,15 @@ def run_sweep(which, kind, steps, warmup):
         ms = st.elapsed_time(en) / steps
         peak = PEAK_TFLOPS[cfg.dtype]
         tf = cfg.flops() / (ms * 1e-3) / 1e12
+        alg = sum(f for _, f in plan.launches())
         rows[name] = {"matrices": cfg.n, "params_M": round(cfg.params() / 1e6, 2),
                       "paper_tflop_per_set": round(cfg.flops() / 1e12, 4), "ms_per_set": round(ms, 4),
                       "weight_sets_per_s": round(1000.0 / ms, 2), "paper_tflops": round(tf, 1),
-                      "frac_of_peak": round(tf / peak, 4), "mfma_flops_per_set": plan.info()["mfma_flops"]}
+                      "paper_frac_of_peak": round(tf / peak, 4),
+                      "alg_tflop_per_set": round(alg / 1e12, 4),
+                      "alg_tflops": round(alg / (ms * 1e-3) / 1e12, 1),
+                      "gram_space_matrices": plan.info()["gram_space"],
+                      "mfma_flops_per_set": plan.info()["mfma_flops"]}
         print(f"[sweep] {name}: {ms:.3f} ms/set, {tf:.0f} TFLOP/s (paper count)", file=sys.stderr, flush=True)
         plan.close()
         del W, G, plan
@@ -285,25 +279,34 @@ def main():
     gpu_vals = vals.cpu().numpy().astype(np.float64)
     print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # per-launch durations, HIP events on the launch stream
-    per_op = {}
+    # per-launch durations, HIP events on the launch stream; the library
+    # reports each launch's kind and algorithmic flops (its products counted
+    # in full on the unpadded shapes)
+    sched = plan.launches()
+    per_op, per_op_flops = {}, {}
     for _ in range(args.profile_steps):
         _, launches = plan.profiled(W, G)
-        for op, t in launches:
+        for (op, t), (op2, fl) in zip(launches, sched):
+            assert op == op2
             per_op.setdefault(op, []).append(t)
+            per_op_flops.setdefault(op, []).append(fl)
     torch.cuda.synchronize()
     gpu_grads = [g.cpu().numpy().astype(np.float64) for g in G]
     op_ms = {op: {"launches_per_step": len(v) // args.profile_steps, "avg_ms": float(np.mean(v)),
-                  "ms_per_step": float(np.sum(v)) / args.profile_steps} for op, v in per_op.items()}
-    dominant = max((op for op in op_ms if op in GEMM_OPS), key=lambda o: op_ms[o]["ms_per_step"])
-    flops = _alg_flops_per_launch(cfg.shapes, dominant)
-    avg_s = op_ms[dominant]["avg_ms"] * 1e-3
-    achieved = flops / avg_s / 1e12
+                  "ms_per_step": float(np.sum(v)) / args.profile_steps,
+                  "alg_flops_per_step": float(np.sum(per_op_flops[op])) / args.profile_steps}
+             for op, v in per_op.items()}
     peak = PEAK_TFLOPS[cfg.dtype]
+    gemm_tflops = {op: round(v["alg_flops_per_step"] / (v["ms_per_step"] * 1e-3) / 1e12, 1)
+                   for op, v in op_ms.items() if op in GEMM_OPS}
+    dominant = max((op for op in op_ms if op in GEMM_OPS), key=lambda o: op_ms[o]["ms_per_step"])
+    d = op_ms[dominant]
+    flops = d["alg_flops_per_step"] / d["launches_per_step"]      # per launch, averaged over the step
+    achieved = d["alg_flops_per_step"] / (d["ms_per_step"] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": _traffic(cfg.name, dominant),
                 "kernel": f"k_gemm<{dominant}>", "alg_flops_per_launch": flops,
-                "avg_launch_ms": op_ms[dominant]["avg_ms"]}
+                "avg_launch_ms": d["avg_ms"], "launches_per_step": d["launches_per_step"]}
 
     hbm = {}
     for op in ("sumsq", "prep", "grad"):
@@ -314,6 +317,7 @@ def main():
 
     value = 1000.0 / ms
     chain_ms = sum(op_ms[o]["ms_per_step"] for o in op_ms if o in GEMM_OPS)
+    chain_alg = sum(op_ms[o]["alg_flops_per_step"] for o in op_ms if o in GEMM_OPS)
     out = {
         "metric": "SLORR-Hoyer fwd+bwd weight-sets/s (ViT-B/16 shapes); % of MFMA peak",
         "value": round(value, 3), "unit": "weight-sets/s", "n_gpus": 1, "steps": args.steps,
@@ -326,6 +330,9 @@ def main():
         "matrices_per_s": round(cfg.n * value, 1),
         "paper_tflops_effective": round(cfg.flops() / (ms * 1e-3) / 1e12, 2),
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
+        "gemm_chain_alg_tflops": round(chain_alg / (chain_ms * 1e-3) / 1e12, 1),
+        "gemm_alg_tflops_by_op": gemm_tflops,
+        "gram_space_matrices": info["gram_space"],
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,
         "integration": None if args.no_integration else integration_timings(cfg, args.kind, W, G, 10),

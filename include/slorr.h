@@ -253,6 +253,15 @@ typedef struct {
 
 SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info);
 
+/* The launch schedule, in launch order: host arrays of
+ * slorr_plan_info_t.launches entries, either may be NULL. ops[i] is the
+ * kernel kind (slorr_op_t) of launch i; alg_flops[i] its algorithmic work:
+ * the products it performs, on the unpadded shapes and counted in full
+ * (2 m n k each, symmetric outputs not halved): A = X X^T 2 P^2 Q, B X and
+ * X_T = M X_0 2 P^2 Q, every P x P product (poly, Gram space) 2 P^3; 0 for
+ * the memory-bound and reduction kernels. Host only. */
+SLORR_API slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops);
+
 /* Name of a status code (static string). */
 SLORR_API const char *slorr_status_string(slorr_status_t status);
 

@@ -34,7 +34,8 @@ OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "g
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",
             "slorr_reg_fwd_bwd_profiled",
-            "slorr_plan_destroy", "slorr_plan_get_info", "slorr_status_string", "slorr_last_error")
+            "slorr_plan_destroy", "slorr_plan_get_info", "slorr_plan_get_launches", "slorr_status_string",
+            "slorr_last_error")
 
 
 class Shape(ctypes.Structure):
@@ -103,6 +104,8 @@ def lib() -> ctypes.CDLL:
         L.slorr_plan_destroy.restype = ctypes.c_int
         L.slorr_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
         L.slorr_plan_get_info.restype = ctypes.c_int
+        L.slorr_plan_get_launches.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
+        L.slorr_plan_get_launches.restype = ctypes.c_int
         L.slorr_status_string.argtypes = [ctypes.c_int]
         L.slorr_status_string.restype = ctypes.c_char_p
         L.slorr_last_error.argtypes = []

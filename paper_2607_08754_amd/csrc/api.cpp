@@ -8,6 +8,7 @@
 #include <stdexcept>
 #include <string>
 #include <utility>
+#include <set>
 #include <vector>
 
 #include "kernels.hpp"
@@ -273,6 +274,37 @@ slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
     info->workspace_bytes = p.ws_bytes;
     info->gram_space = p.gs_count;
     info->m_scale = p.m_scale;
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops) {
+  return guarded([&]() -> slorr_status_t {
+    if (!plan) throw std::invalid_argument("plan is NULL");
+    const slorr::Plan &p = plan->p;
+    for (size_t i = 0; i < p.launches.size(); ++i) {
+      const slorr::Launch &l = p.launches[i];
+      if (ops) ops[i] = int32_t(l.op);
+      if (!alg_flops) continue;
+      const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Sym ||
+                        l.op == slorr::Op::Update || l.op == slorr::Op::Last;
+      double f = 0.0;
+      if (gemm) {
+        std::set<std::pair<int32_t, int32_t>> prods;   // (matrix, product) pairs of the launch
+        for (int k = 0; k < l.grid; ++k) {
+          const slorr::Tile &t = p.tiles[l.tile_first + k];
+          if (t.mat >= 0) prods.insert({t.mat, t.op});
+        }
+        for (const auto &q : prods) {
+          const slorr::MatDesc &d = p.mats[q.first];
+          const double P = d.P, Q = d.Q;
+          const bool pq = (l.op == slorr::Op::Gram && q.second == slorr::kOpXX) ||
+                          ((l.op == slorr::Op::Update || l.op == slorr::Op::Last) && q.second == slorr::kOpBX);
+          f += pq ? 2.0 * P * P * Q : 2.0 * P * P * P;
+        }
+      }
+      alg_flops[i] = f;
+    }
     return SLORR_OK;
   });
 }

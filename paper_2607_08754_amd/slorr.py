@@ -207,6 +207,16 @@ class Plan:
         return out_vals, [(_lib.OPS[ops[i]], float(ms[i])) for i in range(nl)]
 
     # ------------------------------------------------------------------ info
+    def launches(self) -> list:
+        """The schedule in launch order: [(op name, algorithmic flops), ...]
+        (the products each launch performs, counted in full on the unpadded
+        shapes; 0 for the memory-bound kernels)."""
+        nl = self.info()["launches"]
+        ops = (ctypes.c_int32 * max(1, nl))()
+        fl = (ctypes.c_double * max(1, nl))()
+        check(lib().slorr_plan_get_launches(self._handle, ops, fl), "slorr_plan_get_launches")
+        return [(_lib.OPS[ops[i]], float(fl[i])) for i in range(nl)]
+
     def info(self) -> dict:
         inf = _lib.PlanInfo()
         check(lib().slorr_plan_get_info(self._handle, ctypes.byref(inf)), "slorr_plan_get_info")

@@ -131,6 +131,39 @@ def test_plan_facts(L, name):
     assert lib.slorr_plan_destroy(h) == L.OK
 
 
+def test_plan_launch_work(L):
+    """slorr_plan_get_launches: one kind per launch, algorithmic flops of the
+    products each performs. Over a call: X space T (2 P^2 Q + 2 P^3 + 2 P^2 Q)
+    (the paper's count); Gram space 2 P^2 Q (X_0 X_0^T) + T 2 P^3 (poly)
+    + 3 (T - 1) 2 P^3 (C = B A, A = B C, M = B M) + 2 P^2 Q (X_T = M X_0)."""
+    lib = L.lib()
+    for name in ("tiny", "resnet18", "vit_b16", "llm560"):
+        cfg = CONFIGS[name]
+        st, h, _, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER)
+        assert st == L.OK
+        info = L.PlanInfo()
+        lib.slorr_plan_get_info(h, ctypes.byref(info))
+        nl = info.launches
+        ops = (ctypes.c_int32 * nl)()
+        fl = (ctypes.c_double * nl)()
+        assert lib.slorr_plan_get_launches(h, ops, fl) == L.OK
+        names = [L.OPS[o] for o in ops]
+        assert names[:3] == ["sumsq", "norm", "prep"] and names[-3:] == ["finalize", "setsum", "grad"]
+        T = info.iters                                     # the default options: T = 6
+        want = 0.0
+        for m, n in cfg.shapes:
+            P, Q = float(min(m, n)), float(max(m, n))
+            if _pad(int(Q)) >= 2 * _pad(int(P)):
+                want += 4 * P * P * Q + 2 * P ** 3 * (T + 3 * (T - 1))
+            else:
+                want += T * (4 * P * P * Q + 2 * P ** 3)
+        assert sum(fl) == pytest.approx(want, rel=1e-12)
+        assert all(f == 0.0 for f, o in zip(fl, names) if o not in ("gram", "poly", "update", "last", "sym"))
+        assert lib.slorr_plan_get_launches(h, None, None) == L.OK
+        lib.slorr_plan_destroy(h)
+    assert lib.slorr_plan_get_launches(None, None, None) == L.ERR_INVALID_ARGUMENT
+
+
 def test_plan_gram_space_selection(L):
     """Gram space is taken for padded Q >= 2 P and quintic tables only; a cubic
     table, or a table whose M would not fit the fp16 iterate, keeps every
