@@ -70,6 +70,10 @@ struct GemmArgs {
   int use_m;      // update operand is M (Gram space: X_T = M X_0)
   int which_m;    // M buffer: written by a B M product, read by X_T = M X_0
   int store_m;    // poly: also store M_0 = B, scaled by mscale, for Gram-space matrices
+  int store_a0;   // first Gram: also store A_0 for Gram-space matrices
+  int trace_m;    // M = B M_prev: per-tile partials of (f + eps) tr(M A_0) * tscale
+  float tscale;
+  const Scalars *sc;
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
   float alpha, beta, gamma, inv_sx;
@@ -504,6 +508,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // also stores M_0 = B (scaled)
   T *Sym = MODE == kGram ? Am : (tile.op == kOpPoly ? Bm : Cm);
   const bool store_m0 = MODE == kPoly && tile.op == kOpPoly && args.store_m && d.gs;
+  const bool store_a0 = MODE == kGram && tile.op == kOpXX && args.store_a0 && d.gs;
+  // the last M = B M_prev of a Gram-space matrix: trace partials against A_0
+  const bool mtrace = MODE == kUpdate && tile.op == kOpBM && args.trace_m;
   // Symmetric outputs are stored exactly symmetric: off-diagonal tiles also
   // store their transpose; a diagonal tile stores its upper triangle and the
   // transpose of it below the diagonal (its own lower triangle, computed with
@@ -610,6 +617,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= alpha;
           store8_range(Sym + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
+          if (store_a0)
+            store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(grow) * d.Pp + gcol, v,
+                         dtile ? grow - gcol : 0, 8);
         }
       } else if (MODE == kPoly) {
         if (gsp) {
@@ -638,7 +648,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
         }
-        if (MODE == kUpdate && tile.op == kOpBM) store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
+        if (MODE == kUpdate && tile.op == kOpBM) {
+          store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
+          if (mtrace) {
+            float a0[8];
+            load8(reinterpret_cast<const T *>(args.ws + d.a0) + size_t(grow) * d.Pp + gcol, a0);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(a0[j]);
+          }
+        }
         else if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
 #pragma unroll
@@ -671,6 +689,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         if (MODE == kGram || MODE == kPoly) {
           const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
           store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
+          if (store_a0) store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(orow) * d.Pp + ocol, v, 0, hi);
           if (store_m0) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) v[j] *= args.mscale;
@@ -683,9 +702,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       __builtin_amdgcn_wave_barrier();
     }
   }
-  if (MODE == kLast) {
+  if (MODE == kLast || mtrace) {
     __syncthreads();                      // the block sum reuses wave 0's staging area
     const double r = block_sum<NT>(tsum, reinterpret_cast<double *>(smem));
-    if (tid == 0) args.tpart[tile.slot] = r;
+    if (tid == 0) args.tpart[tile.slot] = mtrace ? r * args.sc[tile.mat].feps * double(args.tscale) : r;
   }
 }

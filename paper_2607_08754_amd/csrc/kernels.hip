@@ -325,13 +325,16 @@ template <typename Tx>
 __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict__ tiles,
                                                           const MatDesc *__restrict__ mats,
                                                           char *__restrict__ ws,
-                                                          const float *__restrict__ gpart, float alpha) {
+                                                          const float *__restrict__ gpart, float alpha,
+                                                          int store_a0) {
   constexpr int R = kTile / kRedStripes;          // rows per stripe
   __shared__ float t[R][kTile + 1];
   const Tile e = tiles[blockIdx.x / kRedStripes];
   const int stripe = blockIdx.x % kRedStripes;
   const MatDesc d = mats[e.mat];
   Tx *A = reinterpret_cast<Tx *>(ws + d.a);
+  Tx *A0 = reinterpret_cast<Tx *>(ws + d.a0);    // Gram space: A_0 kept for the trace
+  const bool a0 = store_a0 && d.gs;
   const int m0 = e.tm * kTile + stripe * R, n0 = e.tn * kTile;
   const float *src = gpart + size_t(e.slot) * (kTile * kTile) + stripe * R * kTile;
   for (int q = threadIdx.x; q < R * kTile / 4; q += kThreads) {
@@ -352,14 +355,16 @@ __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = t[r][c + j];
-    Tx *o = A + size_t(m0 + r) * d.Pp + n0 + c;
     const int lo = diag ? (m0 + r) - (n0 + c) : 0;        // upper triangle of a diagonal tile
-    if (lo <= 0) {
-      put8(o, 8, v);
-    } else {
+    for (int k = 0; k < (a0 ? 2 : 1); ++k) {
+      Tx *o = (k ? A0 : A) + size_t(m0 + r) * d.Pp + n0 + c;
+      if (lo <= 0) {
+        put8(o, 8, v);
+      } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j >= lo) o[j] = from_f<Tx>(v[j]);
+        for (int j = 0; j < 8; ++j)
+          if (j >= lo) o[j] = from_f<Tx>(v[j]);
+      }
     }
   }
   // the transpose: R consecutive columns per output row (strictly below the
@@ -369,14 +374,16 @@ __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = t[r + j][c];
-    Tx *o = A + size_t(n0 + c) * d.Pp + m0 + r;
     const int hi = diag ? (n0 + c) - (m0 + r) : 8;
-    if (hi >= 8) {
-      put8(o, 8, v);
-    } else {
+    for (int k = 0; k < (a0 ? 2 : 1); ++k) {
+      Tx *o = (k ? A0 : A) + size_t(n0 + c) * d.Pp + m0 + r;
+      if (hi >= 8) {
+        put8(o, 8, v);
+      } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j < hi) o[j] = from_f<Tx>(v[j]);
+        for (int j = 0; j < 8; ++j)
+          if (j < hi) o[j] = from_f<Tx>(v[j]);
+      }
     }
   }
 }
@@ -582,6 +589,10 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.gamma = l.gamma;
         a.alpha2 = l.alpha2;
         a.mscale = l.mscale;
+        a.store_a0 = l.store_a0;
+        a.trace_m = l.trace_m;
+        a.tscale = l.tscale;
+        a.sc = sc;
         a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
@@ -597,7 +608,7 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         break;
       case Op::GramReduce:
         hipLaunchKernelGGL((k_gram_reduce<Tx>), grid, block, 0, s, tiles + l.tile_first, mats, ws,
-                           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha);
+                           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha, l.store_a0);
         break;
       case Op::SetSum:
         hipLaunchKernelGGL(k_setsum, dim3(1), dim3(1024), 0, s, sc, call, p.n);

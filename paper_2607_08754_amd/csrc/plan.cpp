@@ -108,7 +108,7 @@ void build_plan(Plan &p) {
   }
   // Gram-space iteration, for matrices with Qp >= 2 Pp (see gram_space_scale)
   double sm = 1.0;
-  const bool gs_ok = all_quintic && gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
+  const bool gs_ok = all_quintic && p.iters >= 2 && gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
   p.m_scale = sm;
 
   // canonical shapes, groups
@@ -298,17 +298,18 @@ void build_plan(Plan &p) {
     }
   }
   // Full-output products: the X-space updates (P x Q), in Gram space
-  // M = B M_prev (P x P) and X_T = M X_0 (P x Q). The tiles of the last
-  // product of a matrix (X-space update, X_T = M X_0) own one trace-partial
-  // slot each, contiguous per matrix. The 256-tile needs 256-aligned padded
-  // dims and is used when the launch's 256-tiles still fill the chip twice.
+  // M = B M_prev (P x P) and X_T = M X_0 (P x Q). The tiles of the product
+  // that writes the trace partials of a matrix (its last X-space update; in
+  // Gram space the last M = B M_prev, see Op::Update) own one slot each,
+  // contiguous per matrix. The 256-tile needs 256-aligned padded dims and is
+  // used when the launch has at least min_big of them.
   int32_t slot = 0;
   struct Full {
     int mat;
     int32_t op;
     int32_t n;            // output columns (Qp or Pp)
   };
-  auto full_list = [&](const std::vector<Full> &prods, bool slots, TileRange *out) {
+  auto full_list = [&](const std::vector<Full> &prods, bool slots, int64_t min_big, TileRange *out) {
     int64_t big = 0;
     bool all_big = !prods.empty();
     for (const Full &q : prods) {
@@ -316,7 +317,7 @@ void build_plan(Plan &p) {
       all_big &= d.Pp % kBigTile == 0 && q.n % kBigTile == 0;
       big += int64_t(d.Pp / kBigTile) * (q.n / kBigTile);
     }
-    const int cfg = (all_big && big >= kMinBigTiles) ? kCfg256 : kCfg128;
+    const int cfg = (all_big && big >= min_big) ? kCfg256 : kCfg128;
     std::vector<Job> jobs;
     for (const Full &q : prods) {
       MatDesc &d = p.mats[q.mat];
@@ -347,10 +348,12 @@ void build_plan(Plan &p) {
         mix.push_back({i, kOpBX, d.Qp});
       }
     }
-    full_list(xs, true, p.pq);
-    full_list(fs, true, p.fin);
-    full_list(ms, false, p.mprod);
-    full_list(mix, false, p.pqm);
+    // P x P products (K = Pp) take the 256-tile from one per CU (measured on
+    // ViT-B/16: 432 tiles of 256 beat 1728 of 128)
+    full_list(xs, true, kMinBigTiles, p.pq);
+    full_list(ms, true, kCus, p.mprod);
+    full_list(fs, false, kMinBigTiles, p.fin);
+    full_list(mix, false, kCus, p.pqm);
   }
   p.trace_slots = slot;
   p.chunks.clear();
@@ -399,9 +402,10 @@ void build_plan(Plan &p) {
       d.c = take(pp);
       d.m0 = take(pp);
       d.m1 = take(pp);
+      d.a0 = take(pp);
       d.xt = d.x1;                            // X_T = M X_0 is written to x1
     } else {
-      d.c = d.m0 = d.m1 = d.a;
+      d.c = d.m0 = d.m1 = d.a0 = d.a;
       d.xt = (T & 1) ? d.x1 : d.x0;           // step t reads x[t & 1], writes the other
     }
   }
@@ -440,6 +444,7 @@ void build_plan(Plan &p) {
     g.which_x = wx;
     g.alpha = float(sa / (double(sx) * sx));
     g.alpha2 = prod;
+    g.store_a0 = (t == 0 && p.gs_count) ? 1 : 0;
     if (p.gsplit.count && (t == 0 || !p.gs_count)) {
       g.op = Op::Gram;
       g.grid = p.gsplit.count;
@@ -448,6 +453,7 @@ void build_plan(Plan &p) {
       p.launches.push_back(g);                // fp32 partials
       Launch l = plain(Op::GramReduce, p.gred.count * kRedStripes, p.gred.first);
       l.alpha = g.alpha;
+      l.store_a0 = g.store_a0;
       p.launches.push_back(l);
     } else {
       gemm(Op::Gram, t == 0 ? p.gram : p.gram2, g);
@@ -478,6 +484,11 @@ void build_plan(Plan &p) {
         gemm(Op::Update, p.pqm, u);
       } else {
         gemm(Op::Last, p.pq, u);
+        // the last M writes the trace partials: with X_T = M X_0 and
+        // X_0 = Y / (f + eps), sum(W * P) = (f + eps) tr(X_0^T M X_0) =
+        // (f + eps) tr(M A_0)
+        u.trace_m = 1;
+        u.tscale = float(1.0 / (sm * double(sa)));
         gemm(Op::Update, p.mprod, u);
       }
       // Gram space: C = B A for the next step's A = B C
@@ -494,15 +505,15 @@ void build_plan(Plan &p) {
       gemm(op, p.pq, u);
     }
   }
-  // Gram space: X_T = M_{T-1} X_0, with the trace partials
-  if (p.gs_count) {
+  // Gram space: X_T = M_{T-1} X_0 (the gradient's P; not needed for values only)
+  if (p.gs_count && !(p.flags & SLORR_VALUES_ONLY)) {
     Launch f{};
     f.which_x = 0;
     f.use_m = 1;
     f.which_m = (T - 1) & 1;
     f.fold = 1;
     f.alpha = float(1.0 / sm);
-    gemm(Op::Last, p.fin, f);
+    gemm(Op::Update, p.fin, f);
   }
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
   p.launches.push_back(plain(Op::SetSum, 1));
