@@ -568,25 +568,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     return s;
   };
   if constexpr (MODE == kLast) wprefetch(0, 0);
-  // Poly: the A values of the b A term, likewise one 32-row block ahead
+  // Poly: the A values of the b A term, likewise one 32-row block ahead; the
+  // last M product of a Gram-space matrix: the A_0 values of its trace
   XChunk<T> apre[2][NTASK];
+  const bool apref = (MODE == kPoly && !gsp) || mtrace;
+  const T *asrc = mtrace ? reinterpret_cast<const T *>(args.ws + d.a0) : Am;
   auto aprefetch = [&](int i, int b) {
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
 #pragma unroll
     for (int t = 0; t < NTASK; ++t) {
       const int task = lane + 64 * t;
-      apre[b][t].load(Am + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
+      apre[b][t].load(asrc + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
     }
   };
-  if constexpr (MODE == kPoly)
-    if (!gsp) aprefetch(0, 0);
+  if constexpr (MODE == kPoly || MODE == kUpdate)
+    if (apref) aprefetch(0, 0);
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if constexpr (MODE == kLast)
       if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
-    if constexpr (MODE == kPoly)
-      if (i + 1 < FM && !gsp) aprefetch(i + 1, (i + 1) & 1);
+    if constexpr (MODE == kPoly || MODE == kUpdate)
+      if (i + 1 < FM && apref) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -651,10 +654,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         if (MODE == kUpdate && tile.op == kOpBM) {
           store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
           if (mtrace) {
-            float a0[8];
-            load8(reinterpret_cast<const T *>(args.ws + d.a0) + size_t(grow) * d.Pp + gcol, a0);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(a0[j]);
+            for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(apre[i & 1][t].get(j));
           }
         }
         else if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
