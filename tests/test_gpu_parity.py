@@ -87,6 +87,22 @@ def test_ragged_shapes(dtype, kind):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("iters", [2, 3, 7])
+def test_gram_space_schedules(dtype, iters):
+    """Matrices with padded Q >= 2 P iterate in Gram space (P x P products,
+    X_T = M X_0); short and long schedules (first / middle / last step logic,
+    the M ping-pong parity), both orientations, padding, beside an X-space
+    matrix, both kinds."""
+    shapes = [(96, 300), (300, 96), (128, 512), (250, 260)]
+    arrs = [gaussian(s, seed=23, std=0.05, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+    for kind in ("hoyer", "nuclear"):
+        vals, grads, plan = run_gpu(arrs, dtype, kind, iters, eps=1e-4, g=0.8)
+        assert plan.info()["gram_space"] == 3
+        refs = run_oracle(arrs, dtype, kind, iters, eps=1e-4, g=0.8)
+        compare(vals, grads, refs, kind, dtype, g=0.8, label=f"gram space T={iters} {dtype} {kind}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_split_k_gram_long_rows(dtype):
     """Few Gram tiles with long k ranges: the split-K Gram (parts of unequal
     length when Qp / 128 is not a multiple of the part count) and its reduce."""
