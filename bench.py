@@ -27,6 +27,13 @@ if ROOT not in sys.path:
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA: fp16/bf16 operands, fp32 operands
 GEMM_OPS = ("gram", "poly", "update", "last", "sym")
+# kernel mode of each product launch kind (the C = B A step runs the poly kernel)
+KERNEL_MODE = {"gram": "gram", "poly": "poly", "sym": "poly", "update": "update", "last": "last"}
+
+
+def kernel_instance(op, edge):
+    """Name of the GEMM kernel instance a launch runs: mode and block tile."""
+    return f"k_gemm<{KERNEL_MODE[op]}, {edge}x{edge}>"
 
 
 def _alg_bytes_per_launch(shapes, dtype, op):
@@ -189,7 +196,7 @@ def run_sweep(which, kind, steps, warmup):
         ms = st.elapsed_time(en) / steps
         peak = PEAK_TFLOPS[cfg.dtype]
         tf = cfg.flops() / (ms * 1e-3) / 1e12
-        alg = sum(f for _, f in plan.launches())
+        alg = sum(f for _, f, _ in plan.launches())
         rows[name] = {"matrices": cfg.n, "params_M": round(cfg.params() / 1e6, 2),
                       "paper_tflop_per_set": round(cfg.flops() / 1e12, 4), "ms_per_set": round(ms, 4),
                       "weight_sets_per_s": round(1000.0 / ms, 2), "paper_tflops": round(tf, 1),
@@ -279,34 +286,50 @@ def main():
     gpu_vals = vals.cpu().numpy().astype(np.float64)
     print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # per-launch durations, HIP events on the launch stream; the library
+    # per-launch durations: HIP events on the launch stream that take each
+    # kernel's start and end timestamps; the library
     # reports each launch's kind and algorithmic flops (its products counted
     # in full on the unpadded shapes)
     sched = plan.launches()
     per_op, per_op_flops = {}, {}
+    per_k, per_k_flops = {}, {}
     for _ in range(args.profile_steps):
         _, launches = plan.profiled(W, G)
-        for (op, t), (op2, fl) in zip(launches, sched):
+        for (op, t), (op2, fl, edge) in zip(launches, sched):
             assert op == op2
             per_op.setdefault(op, []).append(t)
             per_op_flops.setdefault(op, []).append(fl)
+            if edge:
+                k = kernel_instance(op, edge)
+                per_k.setdefault(k, []).append(t)
+                per_k_flops.setdefault(k, []).append(fl)
     torch.cuda.synchronize()
     gpu_grads = [g.cpu().numpy().astype(np.float64) for g in G]
-    op_ms = {op: {"launches_per_step": len(v) // args.profile_steps, "avg_ms": float(np.mean(v)),
-                  "ms_per_step": float(np.sum(v)) / args.profile_steps,
-                  "alg_flops_per_step": float(np.sum(per_op_flops[op])) / args.profile_steps}
-             for op, v in per_op.items()}
+
+    def _stats(times, flops):
+        return {op: {"launches_per_step": len(v) // args.profile_steps, "avg_ms": float(np.mean(v)),
+                     "ms_per_step": float(np.sum(v)) / args.profile_steps,
+                     "alg_flops_per_step": float(np.sum(flops[op])) / args.profile_steps}
+                for op, v in times.items()}
+
+    op_ms, k_ms = _stats(per_op, per_op_flops), _stats(per_k, per_k_flops)
     peak = PEAK_TFLOPS[cfg.dtype]
     gemm_tflops = {op: round(v["alg_flops_per_step"] / (v["ms_per_step"] * 1e-3) / 1e12, 1)
                    for op, v in op_ms.items() if op in GEMM_OPS}
-    dominant = max((op for op in op_ms if op in GEMM_OPS), key=lambda o: op_ms[o]["ms_per_step"])
-    d = op_ms[dominant]
+    # the dominant kernel: the GEMM kernel instance (mode and block tile, as a
+    # profiler names it) with the most time per step; its rate is its flops
+    # per launch over its average launch duration
+    dominant = max(k_ms, key=lambda k: k_ms[k]["ms_per_step"])
+    d = k_ms[dominant]
     flops = d["alg_flops_per_step"] / d["launches_per_step"]      # per launch, averaged over the step
-    achieved = d["alg_flops_per_step"] / (d["ms_per_step"] * 1e-3) / 1e12
+    achieved = flops / (d["avg_ms"] * 1e-3) / 1e12
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(achieved / peak, 4), "traffic": _traffic(cfg.name, dominant),
-                "kernel": f"k_gemm<{dominant}>", "alg_flops_per_launch": flops,
+                "kernel": dominant, "alg_flops_per_launch": flops,
                 "avg_launch_ms": d["avg_ms"], "launches_per_step": d["launches_per_step"]}
+    gemm_kernels = {k: {"launches_per_step": v["launches_per_step"], "avg_ms": round(v["avg_ms"], 5),
+                        "alg_tflops": round(v["alg_flops_per_step"] / (v["ms_per_step"] * 1e-3) / 1e12, 1)}
+                    for k, v in k_ms.items()}
 
     hbm = {}
     for op in ("sumsq", "prep", "grad"):
@@ -332,6 +355,7 @@ def main():
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
         "gemm_chain_alg_tflops": round(chain_alg / (chain_ms * 1e-3) / 1e12, 1),
         "gemm_alg_tflops_by_op": gemm_tflops,
+        "gemm_kernels": gemm_kernels,
         "gram_space_matrices": info["gram_space"],
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,

@@ -220,9 +220,10 @@ typedef enum {
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the
- * schedule is enqueued launch by launch (no graph) with a HIP event recorded
- * before and after every launch on `stream`; the call then synchronises that
- * stream and writes each launch's duration in milliseconds to launch_ms and
+ * schedule is enqueued launch by launch on `stream` (no graph), each launch
+ * with a pair of HIP events that take the kernel's own start and end
+ * timestamps (hipExtLaunchKernelGGL); the call then synchronises that stream
+ * and writes each launch's duration in milliseconds to launch_ms and
  * its kind to launch_op (host arrays of slorr_plan_info_t.launches entries;
  * launch_op may be NULL). Not meant for training loops: it blocks the host. */
 SLORR_API slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
@@ -254,13 +255,16 @@ typedef struct {
 SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info);
 
 /* The launch schedule, in launch order: host arrays of
- * slorr_plan_info_t.launches entries, either may be NULL. ops[i] is the
+ * slorr_plan_info_t.launches entries. ops[i] is the
  * kernel kind (slorr_op_t) of launch i; alg_flops[i] its algorithmic work:
  * the products it performs, on the unpadded shapes and counted in full
  * (2 m n k each, symmetric outputs not halved): A = X X^T 2 P^2 Q, B X and
  * X_T = M X_0 2 P^2 Q, every P x P product (poly, Gram space) 2 P^3; 0 for
- * the memory-bound and reduction kernels. Host only. */
-SLORR_API slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops);
+ * the memory-bound and reduction kernels. tile_edge[i] is the block tile edge
+ * of a product launch (128 or 256: the kernel instance a profiler names), 0
+ * for the others. Any of the three arrays may be NULL. Host only. */
+SLORR_API slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops,
+                                                 int32_t *tile_edge);
 
 /* Name of a status code (static string). */
 SLORR_API const char *slorr_status_string(slorr_status_t status);

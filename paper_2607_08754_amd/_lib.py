@@ -104,7 +104,8 @@ def lib() -> ctypes.CDLL:
         L.slorr_plan_destroy.restype = ctypes.c_int
         L.slorr_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]
         L.slorr_plan_get_info.restype = ctypes.c_int
-        L.slorr_plan_get_launches.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double)]
+        L.slorr_plan_get_launches.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(i32)]
         L.slorr_plan_get_launches.restype = ctypes.c_int
         L.slorr_status_string.argtypes = [ctypes.c_int]
         L.slorr_status_string.restype = ctypes.c_char_p

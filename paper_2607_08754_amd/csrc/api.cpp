@@ -278,16 +278,17 @@ slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
   });
 }
 
-slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops) {
+slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *alg_flops, int32_t *tile_edge) {
   return guarded([&]() -> slorr_status_t {
     if (!plan) throw std::invalid_argument("plan is NULL");
     const slorr::Plan &p = plan->p;
     for (size_t i = 0; i < p.launches.size(); ++i) {
       const slorr::Launch &l = p.launches[i];
-      if (ops) ops[i] = int32_t(l.op);
-      if (!alg_flops) continue;
       const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Sym ||
                         l.op == slorr::Op::Update || l.op == slorr::Op::Last;
+      if (ops) ops[i] = int32_t(l.op);
+      if (tile_edge) tile_edge[i] = gemm ? (l.cfg == slorr::kCfg256 ? 256 : 128) : 0;
+      if (!alg_flops) continue;
       double f = 0.0;
       if (gemm) {
         std::set<std::pair<int32_t, int32_t>> prods;   // (matrix, product) pairs of the launch

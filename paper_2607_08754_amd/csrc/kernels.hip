@@ -22,6 +22,7 @@
 //              iterate, in W's orientation, optionally accumulated into the
 //              caller's buffer (App. E.3)
 //   k_apply    W <- W - s G_pre, the decoupled update (App. E.2, Alg. 1)
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <stdexcept>
@@ -502,28 +503,45 @@ void check(hipError_t e, const char *what) {
   if (e != hipSuccess) throw HipError(std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Start and stop events of one timed launch.
+struct EvPair {
+  hipEvent_t start, stop;
+};
+
+// One launch on stream s. With an event pair it goes through
+// hipExtLaunchKernelGGL, whose events take the kernel's own start and end
+// timestamps (the interval a kernel trace reports, without the dispatch gap
+// that an event recorded between two launches adds).
+template <typename... KArgs, typename... Args>
+void go(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const EvPair *ev, Args... args) {
+  if (ev)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, ev->start, ev->stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
+
 template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
-void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s) {
+void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
   switch (op) {
     case Op::Gram:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      go(k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Poly:
     case Op::Sym:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      go(k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Update:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     default:
-      hipLaunchKernelGGL((k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>), grid, block, 0, s, a);
+      go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
   }
 }
 
 template <typename Tw, typename Tx>
-void launch_grad(const Plan &p, const Launch &l, hipStream_t s) {
+void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev) {
   const char *ws = static_cast<const char *>(p.ws);
   const Tile *tiles = reinterpret_cast<const Tile *>(ws + p.off_tiles) + l.tile_first;
   const MatDesc *mats = reinterpret_cast<const MatDesc *>(ws + p.off_mats);
@@ -533,11 +551,9 @@ void launch_grad(const Plan &p, const Launch &l, hipStream_t s) {
   const float inv_sx = 1.0f / (sizeof(Tx) == 2 ? kScaleX16 : 1.0f);
   const int acc = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
   if (p.grad_dtype == SLORR_BF16)
-    hipLaunchKernelGGL((k_grad<Tw, Tx, bf16_t>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
-                       call, ws, inv_sx, acc);
+    go(k_grad<Tw, Tx, bf16_t>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc);
   else
-    hipLaunchKernelGGL((k_grad<Tw, Tx, float>), dim3(l.grid), dim3(kThreads), 0, s, tiles, mats, dyn, sc,
-                       call, ws, inv_sx, acc);
+    go(k_grad<Tw, Tx, float>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc);
 }
 
 template <typename Tw, typename Tx>
@@ -556,16 +572,17 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
   for (size_t li = 0; li < p.launches.size(); ++li) {
     const Launch &l = p.launches[li];
     const dim3 grid(l.grid), block(kThreads);
-    if (events) check(hipEventRecord(events[2 * li], s), "hipEventRecord");
+    const EvPair pair{events ? events[2 * li] : nullptr, events ? events[2 * li + 1] : nullptr};
+    const EvPair *ev = events ? &pair : nullptr;
     switch (l.op) {
       case Op::SumSq:
-        hipLaunchKernelGGL(k_sumsq<Tw>, grid, block, 0, s, chunks, dyn, sumsq);
+        go(k_sumsq<Tw>, grid, block, s, ev, chunks, dyn, sumsq);
         break;
       case Op::NormFin:
-        hipLaunchKernelGGL(k_norm_fin, grid, block, 0, s, mats, sc, sumsq, p.n, p.eps);   // 4 matrices per block
+        go(k_norm_fin, grid, block, s, ev, mats, sc, sumsq, p.n, p.eps);   // 4 matrices per block
         break;
       case Op::Prep:
-        hipLaunchKernelGGL((k_prep<Tw, Tx>), grid, block, 0, s, tiles + l.tile_first, mats, dyn, sc, ws, sx);
+        go(k_prep<Tw, Tx>, grid, block, s, ev, tiles + l.tile_first, mats, dyn, sc, ws, sx);
         break;
       case Op::Gram:
       case Op::Poly:
@@ -597,28 +614,26 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
         if (l.cfg == kCfg256)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev);
         else
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s);
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s, ev);
         break;
       }
       case Op::Finalize:
-        hipLaunchKernelGGL(k_finalize, grid, dim3(64), 0, s, mats, sc, trace, call, p.n, int(p.kind),
-                           (p.flags & SLORR_AUX) ? 1 : 0);
+        go(k_finalize, grid, dim3(64), s, ev, mats, sc, trace, call, p.n, int(p.kind), (p.flags & SLORR_AUX) ? 1 : 0);
         break;
       case Op::GramReduce:
-        hipLaunchKernelGGL((k_gram_reduce<Tx>), grid, block, 0, s, tiles + l.tile_first, mats, ws,
-                           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha, l.store_a0);
+        go(k_gram_reduce<Tx>, grid, block, s, ev, tiles + l.tile_first, mats, ws,
+           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha, l.store_a0);
         break;
       case Op::SetSum:
-        hipLaunchKernelGGL(k_setsum, dim3(1), dim3(1024), 0, s, sc, call, p.n);
+        go(k_setsum, dim3(1), dim3(1024), s, ev, sc, call, p.n);
         break;
       case Op::Grad:
-        launch_grad<Tw, Tx>(p, l, s);
+        launch_grad<Tw, Tx>(p, l, s, ev);
         break;
     }
     check(hipGetLastError(), "kernel launch");
-    if (events) check(hipEventRecord(events[2 * li + 1], s), "hipEventRecord");
   }
 }
 
@@ -652,9 +667,9 @@ void enqueue_apply(const Plan &p, hipStream_t s) {
 void enqueue_grad(const Plan &p, hipStream_t s) {
   if (!p.grad_launch.grid) return;
   if (p.dtype == SLORR_BF16)
-    launch_grad<bf16_t, _Float16>(p, p.grad_launch, s);
+    launch_grad<bf16_t, _Float16>(p, p.grad_launch, s, nullptr);
   else
-    launch_grad<float, float>(p, p.grad_launch, s);
+    launch_grad<float, float>(p, p.grad_launch, s, nullptr);
   check(hipGetLastError(), "kernel launch");
 }
 

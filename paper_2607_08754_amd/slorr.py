@@ -191,8 +191,8 @@ class Plan:
         return weights
 
     def profiled(self, weights, grads=None, grad_scale: float = 1.0, out_vals=None, stream=None):
-        """One call enqueued launch by launch with HIP events around every
-        launch on `stream`; blocks. Returns (out_vals, [(op name, ms), ...])."""
+        """One call enqueued launch by launch on `stream`, each launch timed
+        by HIP events that take the kernel's own start and end; blocks. Returns (out_vals, [(op name, ms), ...])."""
         import torch
         wp, gp, out_vals, stream = self._marshal(weights, grads, out_vals, stream)
         nl = self.info()["launches"]
@@ -208,14 +208,16 @@ class Plan:
 
     # ------------------------------------------------------------------ info
     def launches(self) -> list:
-        """The schedule in launch order: [(op name, algorithmic flops), ...]
-        (the products each launch performs, counted in full on the unpadded
-        shapes; 0 for the memory-bound kernels)."""
+        """The schedule in launch order: [(op name, algorithmic flops, tile
+        edge), ...] (the products each launch performs, counted in full on the
+        unpadded shapes, 0 for the memory-bound kernels; the block tile edge of
+        a product launch, 0 for the others)."""
         nl = self.info()["launches"]
         ops = (ctypes.c_int32 * max(1, nl))()
         fl = (ctypes.c_double * max(1, nl))()
-        check(lib().slorr_plan_get_launches(self._handle, ops, fl), "slorr_plan_get_launches")
-        return [(_lib.OPS[ops[i]], float(fl[i])) for i in range(nl)]
+        te = (ctypes.c_int32 * max(1, nl))()
+        check(lib().slorr_plan_get_launches(self._handle, ops, fl, te), "slorr_plan_get_launches")
+        return [(_lib.OPS[ops[i]], float(fl[i]), int(te[i])) for i in range(nl)]
 
     def info(self) -> dict:
         inf = _lib.PlanInfo()

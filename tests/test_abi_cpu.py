@@ -146,8 +146,11 @@ def test_plan_launch_work(L):
         nl = info.launches
         ops = (ctypes.c_int32 * nl)()
         fl = (ctypes.c_double * nl)()
-        assert lib.slorr_plan_get_launches(h, ops, fl) == L.OK
+        te = (ctypes.c_int32 * nl)()
+        assert lib.slorr_plan_get_launches(h, ops, fl, te) == L.OK
         names = [L.OPS[o] for o in ops]
+        gemm = ("gram", "poly", "update", "last", "sym")
+        assert all((e in (128, 256)) if o in gemm else e == 0 for o, e in zip(names, te))
         assert names[:3] == ["sumsq", "norm", "prep"] and names[-3:] == ["finalize", "setsum", "grad"]
         T = info.iters                                     # the default options: T = 6
         want = 0.0
@@ -158,10 +161,10 @@ def test_plan_launch_work(L):
             else:
                 want += T * (4 * P * P * Q + 2 * P ** 3)
         assert sum(fl) == pytest.approx(want, rel=1e-12)
-        assert all(f == 0.0 for f, o in zip(fl, names) if o not in ("gram", "poly", "update", "last", "sym"))
-        assert lib.slorr_plan_get_launches(h, None, None) == L.OK
+        assert all(f == 0.0 for f, o in zip(fl, names) if o not in gemm)
+        assert lib.slorr_plan_get_launches(h, None, None, None) == L.OK
         lib.slorr_plan_destroy(h)
-    assert lib.slorr_plan_get_launches(None, None, None) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan_get_launches(None, None, None, None) == L.ERR_INVALID_ARGUMENT
 
 
 def test_plan_gram_space_selection(L):
