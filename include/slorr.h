@@ -208,21 +208,21 @@ typedef enum {
   SLORR_OP_SUMSQ = 0,     /* partial sums of W^2 per chunk               */
   SLORR_OP_NORM = 1,      /* ||W||_F and ||W||_F + eps per matrix         */
   SLORR_OP_PREP = 2,      /* X_0 = W / (||W||_F + eps), short-side layout */
-  SLORR_OP_GRAM = 3,      /* A = X X^T                                    */
+  SLORR_OP_GRAM = 3,      /* A = X X^T; Gram space: A = B C               */
   SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
-  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X; Gram space: M = B M_prev    */
+  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X; Gram space: M = B M_prev,   */
+                          /* C = B A, X_T = M X_0                         */
   SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
   SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
-  SLORR_OP_GRAM_REDUCE = 10, /* sum of split-K Gram partials, A = X X^T    */
-  SLORR_OP_SYM = 11       /* Gram space: C = B A                          */
+  SLORR_OP_GRAM_REDUCE = 10  /* sum of split-K Gram partials, A = X X^T    */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the
  * schedule is enqueued launch by launch on `stream` (no graph), each launch
- * with a pair of HIP events that take the kernel's own start and end
- * timestamps (hipExtLaunchKernelGGL); the call then synchronises that stream
+ * with a pair of HIP events (device-scope release) that take the kernel's
+ * start and end timestamps (hipExtLaunchKernelGGL); the call then synchronises that stream
  * and writes each launch's duration in milliseconds to launch_ms and
  * its kind to launch_op (host arrays of slorr_plan_info_t.launches entries;
  * launch_op may be NULL). Not meant for training loops: it blocks the host. */

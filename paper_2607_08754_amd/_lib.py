@@ -28,8 +28,7 @@ NO_GRAPH = 0x4
 AUX = 0x8
 DEFER_GRAD = 0x10
 
-OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce",
-       "sym")
+OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce")
 
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",

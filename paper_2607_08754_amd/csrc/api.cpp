@@ -265,7 +265,7 @@ slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
     int64_t tiles = 0;
     for (const auto &l : p.launches)
       if (l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Update ||
-          l.op == slorr::Op::Last || l.op == slorr::Op::Sym)
+          l.op == slorr::Op::Last)
         tiles += l.grid;
     info->gemm_tiles = tiles;
     info->paper_flops = p.paper_flops;
@@ -284,7 +284,7 @@ slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *
     const slorr::Plan &p = plan->p;
     for (size_t i = 0; i < p.launches.size(); ++i) {
       const slorr::Launch &l = p.launches[i];
-      const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Sym ||
+      const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly ||
                         l.op == slorr::Op::Update || l.op == slorr::Op::Last;
       if (ops) ops[i] = int32_t(l.op);
       if (tile_edge) tile_edge[i] = gemm ? (l.cfg == slorr::kCfg256 ? 256 : 128) : 0;
@@ -448,7 +448,9 @@ slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
           if (x) (void)hipEventDestroy(x);
       }
     } guard{ev};
-    for (auto &e : ev) hip_check(hipEventCreate(&e), "hipEventCreate");
+    // device-scope release: the events add no system-scope cache write-back
+    // to the interval they time (the graph's launches have none either)
+    for (auto &e : ev) hip_check(hipEventCreateWithFlags(&e, hipEventReleaseToDevice), "hipEventCreateWithFlags");
     p.state_ready = false;
     slorr::enqueue(p, s, ev.data());
     p.state_ready = !(p.flags & SLORR_VALUES_ONLY);

@@ -77,7 +77,7 @@ struct GemmArgs {
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
   float alpha, beta, gamma, inv_sx;
-  float alpha2;   // scale of the Gram-space products (A = B C, M = B M, C = B A)
+  float alpha2;   // scale of the Gram-space A = B C
   float mscale;
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
 };
@@ -342,12 +342,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     }
   } else if (MODE == kGram) {                        // A = B C (Gram space)
     Ap = Bm; Bp = Cm; lda = ldb = d.Pp; K = d.Pp;
-  } else if (MODE == kPoly) {                        // A A, or B A (Gram space)
-    Ap = tile.op == kOpPoly ? Am : Bm;
-    Bp = Am;
-    lda = ldb = d.Pp; K = d.Pp;
+  } else if (MODE == kPoly) {                        // A A
+    Ap = Am; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
   } else if (tile.op == kOpBM) {                     // M = B M_prev (Gram space)
     Ap = Bm; Bp = Mr; lda = ldb = d.Pp; K = d.Pp;
+  } else if (tile.op == kOpBA) {                     // C = B A (Gram space)
+    Ap = Bm; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
   } else {                                           // B X, A X, or M X_0
     Ap = args.use_m ? Mw : (args.use_a ? Am : Bm); Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
   }
@@ -501,12 +501,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
-  // Gram-space products scale by alpha2; the poly adds b A + a I
-  const bool gsp = (MODE == kGram || MODE == kPoly) && tile.op != 0;
+  // Gram-space A = B C scales by alpha2; the poly adds b A + a I
+  const bool gsp = MODE == kGram && tile.op == kOpBC;
   const float alpha = gsp ? args.alpha2 : args.alpha, beta = args.beta;
   // symmetric output and where it goes; the first poly of a Gram-space matrix
   // also stores M_0 = B (scaled)
-  T *Sym = MODE == kGram ? Am : (tile.op == kOpPoly ? Bm : Cm);
+  T *Sym = MODE == kGram ? Am : (MODE == kPoly ? Bm : Cm);
   const bool store_m0 = MODE == kPoly && tile.op == kOpPoly && args.store_m && d.gs;
   const bool store_a0 = MODE == kGram && tile.op == kOpXX && args.store_a0 && d.gs;
   // the last M = B M_prev of a Gram-space matrix: trace partials against A_0
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // a different rounding, is not used). The Gram-space products need this:
   // with operands symmetric only up to rounding, B Y^T (the NT product) and
   // B Y drift apart over the steps.
-  const bool mirror = (MODE == kGram || MODE == kPoly) && !part;
+  const bool mirror = ((MODE == kGram || MODE == kPoly) && !part) || (MODE == kUpdate && tile.op == kOpBA);
   const bool dtile = mirror && tile.tm == tile.tn;
   const bool colwise = mirror || (MODE == kLast && d.tall);
   double tsum = 0.0;
@@ -571,7 +571,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // Poly: the A values of the b A term, likewise one 32-row block ahead; the
   // last M product of a Gram-space matrix: the A_0 values of its trace
   XChunk<T> apre[2][NTASK];
-  const bool apref = (MODE == kPoly && !gsp) || mtrace;
+  const bool apref = MODE == kPoly || mtrace;
   const T *asrc = mtrace ? reinterpret_cast<const T *>(args.ws + d.a0) : Am;
   auto aprefetch = [&](int i, int b) {
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
@@ -625,14 +625,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
                          dtile ? grow - gcol : 0, 8);
         }
       } else if (MODE == kPoly) {
-        if (gsp) {
 #pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] *= alpha;
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j)
-            v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
-        }
+        for (int j = 0; j < 8; ++j)
+          v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
         const int lo = dtile ? grow - gcol : 0;
         store8_range(Sym + size_t(grow) * d.Pp + gcol, v, lo, 8);
         if (store_m0) {
@@ -657,8 +652,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(apre[i & 1][t].get(j));
           }
+        } else if (MODE == kUpdate && tile.op == kOpBA) {
+          store8_range(Cm + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
+        } else if (MODE == kUpdate || args.write_x) {
+          store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         }
-        else if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
@@ -687,7 +685,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = ep[(rg * 8 + j) * P + col];
         const int orow = gcol0 + col, ocol = grow0 + rg * 8;
-        if (MODE == kGram || MODE == kPoly) {
+        if (MODE == kGram || MODE == kPoly || MODE == kUpdate) {
           const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
           store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
           if (store_a0) store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(orow) * d.Pp + ocol, v, 0, hi);

@@ -528,7 +528,6 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPai
       go(k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Poly:
-    case Op::Sym:
       go(k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Update:
@@ -586,7 +585,6 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         break;
       case Op::Gram:
       case Op::Poly:
-      case Op::Sym:
       case Op::Update:
       case Op::Last: {
         GemmArgs a;

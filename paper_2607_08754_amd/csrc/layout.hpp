@@ -66,11 +66,12 @@ struct Tile {                  // one GEMM output tile / one prep tile / one Gra
 
 // Product of a GEMM tile. Gram launches (symmetric output): A = X X^T
 // (kOpXX) or, in Gram space, A = B C (kOpBC). Poly launches (symmetric
-// output): B = poly(A) (kOpPoly) or, in Gram space, C = B A (kOpBA). Update
-// launches (full output): X' = B X (kOpBX) or, in Gram space, M = B M_prev
-// (kOpBM), which is not symmetrised: B and M_prev commute only up to the
-// rounding of earlier steps.
-enum TileOp : int32_t { kOpXX = 0, kOpBC = 1, kOpPoly = 0, kOpBA = 1, kOpBX = 0, kOpBM = 1 };
+// output): B = poly(A) (kOpPoly). Update launches: X' = B X (kOpBX) and, in
+// Gram space, M = B M_prev (kOpBM; full output, not symmetrised: B and
+// M_prev commute only up to the rounding of earlier steps) and C = B A
+// (kOpBA; symmetric output on upper tiles, A read as its own transpose, which
+// it is exactly).
+enum TileOp : int32_t { kOpXX = 0, kOpBC = 1, kOpPoly = 0, kOpBX = 0, kOpBM = 1, kOpBA = 2 };
 
 struct Chunk {                 // a contiguous run of a matrix's elements
   int32_t mat, begin, len, pad;

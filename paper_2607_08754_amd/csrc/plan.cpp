@@ -201,7 +201,7 @@ void build_plan(Plan &p) {
     return r;
   };
 
-  // Symmetric-output products (Gram, poly, Gram-space products): upper-
+  // Symmetric-output products of the Gram and poly launches: upper-
   // triangle tiles only; the kernel also stores the transpose of off-diagonal
   // tiles. `prods` lists the products of one launch as (matrix, op, k extent);
   // the 256-tile is used for every product of the launch when all of them
@@ -240,20 +240,17 @@ void build_plan(Plan &p) {
   // the set has one upper-triangle 256-tile per CU. The P x P products
   // (K = Pp, the shortest) take it only with two per CU.
   {
-    std::vector<Prod> g0, g1, pl, c0;
+    std::vector<Prod> g0, g1, pl;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
       g0.push_back({i, kOpXX, d.Qp});
       g1.push_back(d.gs ? Prod{i, kOpBC, d.Pp} : Prod{i, kOpXX, d.Qp});
       pl.push_back({i, kOpPoly, d.Pp});
-      if (d.gs) c0.push_back({i, kOpBA, d.Pp});
     }
     sym_list(g0, kCus, p.gram);
     if (p.gs_count && T > 1) sym_list(g1, kMinBigTiles, p.gram2);
     else std::copy(p.gram, p.gram + kNumCfg, p.gram2);
     sym_list(pl, kMinBigTiles, p.pp);
-    for (int c = 0; c < kNumCfg; ++c) p.sym_c[c] = TileRange{};
-    if (p.gs_count && T > 1) sym_list(c0, kMinBigTiles, p.sym_c);
   }
   // Split-K Gram. A set with few Gram tiles (small P) but long K = Qp would
   // leave most CUs idle: every tile's k range is cut into parts (multiples of
@@ -297,60 +294,74 @@ void build_plan(Plan &p) {
       p.gred.count = int32_t(reds.size());
     }
   }
-  // Full-output products: the X-space updates (P x Q), in Gram space
-  // M = B M_prev (P x P) and X_T = M X_0 (P x Q). The tiles of the product
+  // Update launches: the X-space updates B X (P x Q), in Gram space
+  // M = B M_prev (P x P) and X_T = M X_0 (P x Q), all full outputs, and
+  // C = B A (P x P, upper tiles, stored mirrored). The tiles of the product
   // that writes the trace partials of a matrix (its last X-space update; in
   // Gram space the last M = B M_prev, see Op::Update) own one slot each,
-  // contiguous per matrix. The 256-tile needs 256-aligned padded dims and is
-  // used when the launch has at least min_big of them.
+  // contiguous per matrix. A matrix's products form one job, row band by row
+  // band (every product of a band reads the same rows of B). The 256-tile
+  // needs 256-aligned padded dims and is used when the launch has at least
+  // min_big of them.
   int32_t slot = 0;
   struct Full {
     int mat;
     int32_t op;
     int32_t n;            // output columns (Qp or Pp)
+    bool upper;           // symmetric output: upper tiles only
   };
   auto full_list = [&](const std::vector<Full> &prods, bool slots, int64_t min_big, TileRange *out) {
     int64_t big = 0;
     bool all_big = !prods.empty();
     for (const Full &q : prods) {
       const MatDesc &d = p.mats[q.mat];
+      const int64_t nb = d.Pp / kBigTile, mb = q.n / kBigTile;
       all_big &= d.Pp % kBigTile == 0 && q.n % kBigTile == 0;
-      big += int64_t(d.Pp / kBigTile) * (q.n / kBigTile);
+      big += q.upper ? nb * (nb + 1) / 2 : nb * mb;
     }
     const int cfg = (all_big && big >= min_big) ? kCfg256 : kCfg128;
+    const int ts = tsize(cfg);
     std::vector<Job> jobs;
-    for (const Full &q : prods) {
-      MatDesc &d = p.mats[q.mat];
-      Job j{q.mat, double(d.Pp), {}};
+    for (size_t f = 0; f < prods.size();) {
+      size_t e = f;                                // products f .. e-1: one matrix
+      while (e < prods.size() && prods[e].mat == prods[f].mat) ++e;
+      MatDesc &d = p.mats[prods[f].mat];
+      Job j{prods[f].mat, double(d.Pp), {}};
       if (slots) d.trace_begin = slot;
-      for (int tm = 0; tm < d.Pp / tsize(cfg); ++tm)
-        for (int tn = 0; tn < q.n / tsize(cfg); ++tn) {
-          Tile t = make_tile(q.mat, tm, tn, slots ? slot++ : 0);
-          t.op = q.op;
-          j.tiles.push_back(t);
-        }
+      for (int tm = 0; tm < d.Pp / ts; ++tm)
+        for (size_t q = f; q < e; ++q)
+          for (int tn = prods[q].upper ? tm : 0; tn < prods[q].n / ts; ++tn) {
+            Tile t = make_tile(prods[q].mat, tm, tn, slots ? slot++ : 0);
+            t.op = prods[q].op;
+            j.tiles.push_back(t);
+          }
       if (slots) d.trace_end = slot;
       jobs.push_back(std::move(j));
+      f = e;
     }
     for (int c = 0; c < kNumCfg; ++c) out[c] = TileRange{};
     out[cfg] = emit(std::move(jobs));
   };
   {
-    std::vector<Full> xs, mix, ms, fs;
+    std::vector<Full> xs, first, mix, ms, fs;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
       if (d.gs) {
-        mix.push_back({i, kOpBM, d.Pp});
-        ms.push_back({i, kOpBM, d.Pp});
-        fs.push_back({i, kOpBX, d.Qp});
+        first.push_back({i, kOpBA, d.Pp, true});
+        mix.push_back({i, kOpBM, d.Pp, false});
+        mix.push_back({i, kOpBA, d.Pp, true});
+        ms.push_back({i, kOpBM, d.Pp, false});
+        fs.push_back({i, kOpBX, d.Qp, false});
       } else {
-        xs.push_back({i, kOpBX, d.Qp});
-        mix.push_back({i, kOpBX, d.Qp});
+        xs.push_back({i, kOpBX, d.Qp, false});
+        first.push_back({i, kOpBX, d.Qp, false});
+        mix.push_back({i, kOpBX, d.Qp, false});
       }
     }
     // P x P products (K = Pp) take the 256-tile from one per CU (measured on
     // ViT-B/16: 432 tiles of 256 beat 1728 of 128)
     full_list(xs, true, kMinBigTiles, p.pq);
+    full_list(first, false, kCus, p.pqc);
     full_list(ms, true, kCus, p.mprod);
     full_list(fs, false, kMinBigTiles, p.fin);
     full_list(mix, false, kCus, p.pqm);
@@ -478,8 +489,11 @@ void build_plan(Plan &p) {
       u.which_m = t & 1;
       u.fold = 1;
       u.alpha = prod;
-      if (t == 0 || !p.gs_count) {
+      // and C = B A for the next step's A = B C (t < T - 1)
+      if (!p.gs_count) {
         gemm(op, p.pq, u);
+      } else if (t == 0 && T > 1) {
+        gemm(Op::Update, p.pqc, u);
       } else if (t < T - 1) {
         gemm(Op::Update, p.pqm, u);
       } else {
@@ -491,10 +505,6 @@ void build_plan(Plan &p) {
         u.tscale = float(1.0 / (sm * double(sa)));
         gemm(Op::Update, p.mprod, u);
       }
-      // Gram space: C = B A for the next step's A = B C
-      Launch sp{};
-      sp.alpha2 = prod;
-      if (p.gs_count && t < T - 1) gemm(Op::Sym, p.sym_c, sp);
     } else {
       // cubic step (no Gram-space matrices): X'_s = a X_s + b (A_s X_s) / s_a
       Launch u{};
@@ -527,8 +537,7 @@ void build_plan(Plan &p) {
   // MFMA work the launches execute (padded, symmetric tiles counted once)
   p.mfma_flops = 0;
   for (const Launch &l : p.launches) {
-    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last && l.op != Op::Sym)
-      continue;
+    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last) continue;
     const double ts = tsize(l.cfg);
     for (int k = 0; k < l.grid; ++k) {
       const Tile &tl = p.tiles[l.tile_first + k];

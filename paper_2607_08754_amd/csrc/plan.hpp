@@ -26,8 +26,7 @@ enum class Op : int {
   Finalize = SLORR_OP_FINALIZE,  // values and gradient factors, one block per matrix
   Grad = SLORR_OP_GRAD,          // grad = g (s1 P - s2 W)   (original orientation)
   SetSum = SLORR_OP_SETSUM,      // set total in index order
-  GramReduce = SLORR_OP_GRAM_REDUCE,  // A = sum of the split-K Gram partials
-  Sym = SLORR_OP_SYM             // Gram space: C = B A
+  GramReduce = SLORR_OP_GRAM_REDUCE   // A = sum of the split-K Gram partials
 };
 
 // GEMM block-tile configurations (kernel template instances).
@@ -51,7 +50,7 @@ struct Launch {
   int32_t trace_m;     // last M = B M_prev: trace partials of M A_0 (Gram space)
   int32_t fold;        // update: a_t I already folded into B (no a X term)
   float alpha, beta, gamma;  // epilogue coefficients
-  float alpha2;        // Gram-space products (A = B C, M = B M, C = B A)
+  float alpha2;        // Gram-space A = B C
   float mscale;        // poly: scale of the stored M_0 relative to B
   float tscale;        // trace_m: 1 / (s_m s_a), the scales of M and A_0
 };
@@ -80,10 +79,10 @@ struct Plan {
   TileRange gram2[kNumCfg];                  // A of later steps: X X^T or (Gram space) B C
   TileRange pp[kNumCfg];                     // P x P poly outputs, per GemmCfg
   TileRange pq[kNumCfg];                     // P x Q outputs (update, last) of X-space matrices
-  TileRange pqm[kNumCfg];                    // X-space updates and Gram-space M = B M_prev
-  TileRange mprod[kNumCfg];                  // Gram space: M = B M_prev
+  TileRange pqc[kNumCfg];                    // first step: X-space updates and Gram-space C = B A
+  TileRange pqm[kNumCfg];                    // later steps: also Gram-space M = B M_prev
+  TileRange mprod[kNumCfg];                  // Gram space: the last M = B M_prev
   TileRange fin[kNumCfg];                    // Gram space: X_T = M X_0
-  TileRange sym_c[kNumCfg];                  // Gram space: C = B A
   int32_t gs_count = 0;                      // matrices iterated in Gram space
   double m_scale = 1.0;                      // scale of M in the iterate type
   TileRange prep;                      // prep tiles over Pp x Qp

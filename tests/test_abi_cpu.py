@@ -77,8 +77,11 @@ def _expected_mfma(shapes, T):
     """MFMA work of the schedule. Symmetric products (A, B, C) run on upper-
     triangle tiles: 256 x 256 when every matrix of the launch is 256-aligned
     and the launch has one such tile per CU for X_0 X_0^T, two per CU for the
-    other launches; full products (B X, M = B M_prev, X_T = M X_0) on all
-    tiles. Matrices with padded Q >= 2 P iterate in Gram space."""
+    later A and the poly; full products (B X, M = B M_prev, X_T = M X_0) on all
+    tiles. C = B A runs in the update launch of its step (with the X-space
+    B X and, after the first step, M = B M_prev), whose tiles are 256 x 256
+    when all its products allow it and it has one per CU. Matrices with
+    padded Q >= 2 P iterate in Gram space."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
     gs = [Q >= 2 * P for P, Q in mats]
 
@@ -93,8 +96,16 @@ def _expected_mfma(shapes, T):
     if gps and T > 1:
         t1 = cfg(ps, 512)
         tot += (T - 1) * sum(2 * _tri(P, t1) * (P if g else Q) for (P, Q), g in zip(mats, gs))
-        tc = cfg(gps, 512)
-        tot += (T - 1) * sum(2 * _tri(P, tc) * P for P in gps)          # C = B A
+        def ucfg(prods):                       # (P, output columns, upper) of one update launch
+            big = sum((P // 256) * (P // 256 + 1) // 2 if up else (P // 256) * (N // 256) for P, N, up in prods)
+            ok = all(P % 256 == 0 and N % 256 == 0 for P, N, _ in prods)
+            return 256 if ok and big >= 256 else 128
+        sq = [(P, Q, False) for (P, Q), g in zip(mats, gs) if not g]
+        c = [(P, P, True) for P in gps]
+        tc0 = ucfg(sq + c)
+        tcm = ucfg(sq + [(P, P, False) for P in gps] + c)
+        tot += sum(2 * _tri(P, tc0) * P for P in gps)                   # C = B A, first step
+        tot += (T - 2) * sum(2 * _tri(P, tcm) * P for P in gps)         # C = B A, later steps
         tot += (T - 1) * sum(2.0 * P ** 3 for P in gps)                  # M = B M_prev
     else:
         tot += (T - 1) * sum(2 * _tri(P, t0) * Q for P, Q in mats)
@@ -149,7 +160,7 @@ def test_plan_launch_work(L):
         te = (ctypes.c_int32 * nl)()
         assert lib.slorr_plan_get_launches(h, ops, fl, te) == L.OK
         names = [L.OPS[o] for o in ops]
-        gemm = ("gram", "poly", "update", "last", "sym")
+        gemm = ("gram", "poly", "update", "last")
         assert all((e in (128, 256)) if o in gemm else e == 0 for o, e in zip(names, te))
         assert names[:3] == ["sumsq", "norm", "prep"] and names[-3:] == ["finalize", "setsum", "grad"]
         T = info.iters                                     # the default options: T = 6
@@ -412,8 +423,11 @@ def test_split_k_gram_plan(L):
     info = facts(gs)
     assert info.gram_space == 3
     # first step: gram parts, reduce, poly, C = B A; later steps: A = B C, poly,
-    # M = B M_prev, C = B A (not in the last step); then X_T = M X_0
-    assert info.launches == 3 + 4 + 4 * (T - 2) + 3 + 1 + 3
+    # one update launch with M = B M_prev and C = B A (no C in the last step);
+    # then X_T = M X_0
+    assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 1 + 3
     assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T)[0], rel=1e-12)
-    big = facts(CONFIGS["vit_b16"].shapes)                  # no split: A, poly, B X, B M / B A
-    assert big.launches == 3 + 4 * 6 + 1 + 3
+    # no split: per step A, poly, one update launch (B X, B M, B A); the last
+    # step's X-space update (with the trace against W) is a launch of its own
+    big = facts(CONFIGS["vit_b16"].shapes)
+    assert big.launches == 3 + 3 * 6 + 1 + 1 + 3
