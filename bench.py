@@ -26,9 +26,9 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA: fp16/bf16 operands, fp32 operands
-GEMM_OPS = ("gram", "poly", "update", "last")
+GEMM_OPS = ("gram", "poly", "update", "last", "grad_prod")
 # kernel mode of each product launch kind
-KERNEL_MODE = {"gram": "gram", "poly": "poly", "update": "update", "last": "last"}
+KERNEL_MODE = {"gram": "gram", "poly": "poly", "update": "update", "last": "last", "grad_prod": "grad"}
 
 
 def kernel_instance(op, edge):

@@ -216,7 +216,8 @@ typedef enum {
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
   SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
-  SLORR_OP_GRAM_REDUCE = 10  /* sum of split-K Gram partials, A = X X^T    */
+  SLORR_OP_GRAM_REDUCE = 10, /* sum of split-K Gram partials, A = X X^T    */
+  SLORR_OP_GRAD_PROD = 11 /* Gram space: gradient g (s1 M X_0 - s2 W)      */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the

@@ -28,7 +28,8 @@ NO_GRAPH = 0x4
 AUX = 0x8
 DEFER_GRAD = 0x10
 
-OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce")
+OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce",
+       "grad_prod")
 
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",

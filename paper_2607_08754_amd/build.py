@@ -8,6 +8,7 @@ paper_2607_08754_amd/libslorr.so (replaced atomically).
 from __future__ import annotations
 
 import os
+import re
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -34,9 +35,24 @@ COMMON = [
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     cmd = [HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+    if src.endswith(".hip"):
+        cmd.append("-Rpass-analysis=kernel-resource-usage")
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{res.stdout}\n{res.stderr}")
+    if src.endswith(".hip"):
+        # a kernel whose private arrays or registers went to scratch memory
+        # runs several times slower: refuse the build
+        name, bad = None, []
+        for line in res.stderr.splitlines():
+            m = re.search(r"Function Name: (\S+)", line)
+            if m:
+                name = m.group(1)
+            m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+            if m and int(m.group(1)) > 0:
+                bad.append(f"{name}: {m.group(1)} bytes/lane")
+        if bad:
+            raise RuntimeError("kernels use scratch memory:\n" + "\n".join(bad))
     return obj
 
 

@@ -265,7 +265,7 @@ slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info) {
     int64_t tiles = 0;
     for (const auto &l : p.launches)
       if (l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Update ||
-          l.op == slorr::Op::Last)
+          l.op == slorr::Op::Last || l.op == slorr::Op::GradProd)
         tiles += l.grid;
     info->gemm_tiles = tiles;
     info->paper_flops = p.paper_flops;
@@ -284,8 +284,8 @@ slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *
     const slorr::Plan &p = plan->p;
     for (size_t i = 0; i < p.launches.size(); ++i) {
       const slorr::Launch &l = p.launches[i];
-      const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly ||
-                        l.op == slorr::Op::Update || l.op == slorr::Op::Last;
+      const bool gemm = l.op == slorr::Op::Gram || l.op == slorr::Op::Poly || l.op == slorr::Op::Update ||
+                        l.op == slorr::Op::Last || l.op == slorr::Op::GradProd;
       if (ops) ops[i] = int32_t(l.op);
       if (tile_edge) tile_edge[i] = gemm ? (l.cfg == slorr::kCfg256 ? 256 : 128) : 0;
       if (!alg_flops) continue;
@@ -300,7 +300,8 @@ slorr_status_t slorr_plan_get_launches(slorr_plan_t plan, int32_t *ops, double *
           const slorr::MatDesc &d = p.mats[q.first];
           const double P = d.P, Q = d.Q;
           const bool pq = (l.op == slorr::Op::Gram && q.second == slorr::kOpXX) ||
-                          ((l.op == slorr::Op::Update || l.op == slorr::Op::Last) && q.second == slorr::kOpBX);
+                          ((l.op == slorr::Op::Update || l.op == slorr::Op::Last || l.op == slorr::Op::GradProd) &&
+                           q.second == slorr::kOpBX);
           f += pq ? 2.0 * P * P * Q : 2.0 * P * P * P;
         }
       }

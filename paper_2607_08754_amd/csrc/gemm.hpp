@@ -57,7 +57,10 @@ template <> struct Mfma<float> {
   }
 };
 
-enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2, kLast = 3 };
+// kGrad / kGradB: the Gram-space gradient, g (s1 P - s2 W) with P = M X_0
+// formed tile by tile and written straight into the caller's fp32 / bf16
+// gradient (W's orientation)
+enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2, kLast = 3, kGrad = 4, kGradB = 5 };
 
 struct GemmArgs {
   const Tile *tiles;
@@ -80,6 +83,8 @@ struct GemmArgs {
   float alpha2;   // scale of the Gram-space A = B C
   float mscale;
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
+  const CallParams *call;   // Grad: upstream factors
+  int accumulate; // Grad: add into the gradient buffers
 };
 
 template <int BM, int BN, int WGM, int WGN>
@@ -157,6 +162,29 @@ __device__ __forceinline__ void lds_dma_wait() {
 }
 
 // sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
+// Gradient run of nv elements at g: u = fl(gsc fl(s1 p - s2 w)) (u rounded to
+// bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
+// contraction, the rounding the gradient kernel uses.
+template <typename Tg>
+__device__ __forceinline__ void grad8(Tg *g, int nv, const float (&p)[8], const float (&w)[8], float s1,
+                                      float s2, float gsc, int accumulate) {
+#pragma clang fp contract(off)
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float t = s1 * p[j] - s2 * w[j];
+    v[j] = gsc * t;
+    if constexpr (sizeof(Tg) == 2) v[j] = to_f(from_f<Tg>(v[j]));
+  }
+  if (accumulate) {
+    float old[8];
+    get8(g, nv, old);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = old[j] + v[j];
+  }
+  put8(g, nv, v);
+}
+
 template <typename Tw>
 __device__ __forceinline__ double dot_w(const Tw *w, const float (&v)[8], int n) {
   float wv[8];
@@ -298,7 +326,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int V = Mfma<T>::V;
   constexpr int BK = 8 * V;                      // k per slab (128-byte rows)
   constexpr int FM = S::FM, FN = S::FN, WTM = S::WTM, WTN = S::WTN;
-  constexpr bool KN = (MODE == kUpdate || MODE == kLast);
+  constexpr bool GR = MODE == kGrad || MODE == kGradB;
+  constexpr bool KN = (MODE == kUpdate || MODE == kLast || GR);
   // fp16 [k][n] operand: global -> LDS directly in its own layout, transposed
   // on the LDS read; fp32 goes through registers and is stored transposed
   constexpr bool TR = KN && sizeof(T) == 2;
@@ -519,9 +548,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // B Y drift apart over the steps.
   const bool mirror = ((MODE == kGram || MODE == kPoly) && !part) || (MODE == kUpdate && tile.op == kOpBA);
   const bool dtile = mirror && tile.tm == tile.tn;
+  constexpr bool WR = MODE == kLast || GR;    // the epilogue reads W
   const bool colwise = mirror || (MODE == kLast && d.tall);
   double tsum = 0.0;
-  const Tw *W = (MODE == kLast) ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
+  const Tw *W = WR ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
 
   // Last: the weights each lane multiplies into the trace are known before
   // the accumulators are staged, so they are loaded one 32-row block ahead
@@ -567,7 +597,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wpre[b][t].get(j));
     return s;
   };
-  if constexpr (MODE == kLast) wprefetch(0, 0);
+  if constexpr (WR) wprefetch(0, 0);
   // Poly: the A values of the b A term, likewise one 32-row block ahead; the
   // last M product of a Gram-space matrix: the A_0 values of its trace
   XChunk<T> apre[2][NTASK];
@@ -586,7 +616,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
-    if constexpr (MODE == kLast)
+    if constexpr (WR)
       if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
     if constexpr (MODE == kPoly || MODE == kUpdate)
       if (i + 1 < FM && apref) aprefetch(i + 1, (i + 1) & 1);
@@ -598,6 +628,45 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     // performed in order: a wave-level barrier (no reordering) suffices
     __builtin_amdgcn_wave_barrier();
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
+    if constexpr (GR) {
+      // g (s1 P - s2 W) straight from the staged block, in W's orientation:
+      // runs of 8 along W's rows (canonical rows of a wide W, canonical
+      // columns of a tall one), the tasks wtask and the W prefetch use
+      typedef typename std::conditional<MODE == kGradB, bf16_t, float>::type Tg;
+      Tg *G = static_cast<Tg *>(args.dyn[tile.mat].g);
+      const float s1 = float(args.sc[tile.mat].s1) * args.inv_sx, s2 = float(args.sc[tile.mat].s2);
+      const float gsc = args.call->gscale ? args.call->grad_scale * args.call->gscale[tile.mat]
+                                          : args.call->grad_scale;
+#pragma unroll
+      for (int t = 0; t < NTASK; ++t) {
+        const int task = lane + 64 * t;
+        const Tw *ptr;
+        int nv;
+        if (!wtask(i, t, ptr, nv)) continue;
+        float v[8], wv[8];
+        if (!d.tall) {
+          const float4v *e = reinterpret_cast<const float4v *>(ep + (task / CG) * P + (task % CG) * 8);
+          const float4v e0 = e[0], e1 = e[1];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            v[j] = e0[j] * alpha;
+            v[4 + j] = e1[j] * alpha;
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = ep[((task & 3) * 8 + j) * P + (task >> 2)] * alpha;
+        }
+        if (wfull[i & 1][t]) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) wv[j] = wpre[i & 1][t].get(j);
+        } else {
+          get8(ptr, nv, wv);
+        }
+        grad8(G + (ptr - W), nv, v, wv, s1, s2, gsc, args.accumulate);
+      }
+      __builtin_amdgcn_wave_barrier();
+      continue;
+    }
 #pragma unroll
     for (int t = 0; t < NTASK; ++t) {
       const int task = lane + 64 * t;
@@ -654,7 +723,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
           }
         } else if (MODE == kUpdate && tile.op == kOpBA) {
           store8_range(Cm + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
-        } else if (MODE == kUpdate || args.write_x) {
+        } else if (MODE == kUpdate || (MODE == kLast && args.write_x)) {
           store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         }
         if (MODE == kLast) {

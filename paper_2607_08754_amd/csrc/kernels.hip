@@ -521,7 +521,7 @@ void go(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const Ev
 }
 
 template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
-void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev) {
+void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev, bool grad_bf16) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
   switch (op) {
     case Op::Gram:
@@ -532,6 +532,12 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPai
       break;
     case Op::Update:
       go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      break;
+    case Op::GradProd:
+      if (grad_bf16)
+        go(k_gemm<Tx, Tw, kGradB, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      else
+        go(k_gemm<Tx, Tw, kGrad, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     default:
       go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
@@ -556,7 +562,7 @@ void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev
 }
 
 template <typename Tw, typename Tx>
-void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
+void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev) {
   char *ws = static_cast<char *>(p.ws);
   const MatDesc *mats = reinterpret_cast<const MatDesc *>(ws + p.off_mats);
   const DynDesc *dyn = reinterpret_cast<const DynDesc *>(ws + p.off_dyn);
@@ -568,11 +574,8 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
   double *trace = reinterpret_cast<double *>(ws + p.off_trace);
   const bool f16 = sizeof(Tx) == 2;
   const float sx = f16 ? kScaleX16 : 1.0f;
-  for (size_t li = 0; li < p.launches.size(); ++li) {
-    const Launch &l = p.launches[li];
+  {
     const dim3 grid(l.grid), block(kThreads);
-    const EvPair pair{events ? events[2 * li] : nullptr, events ? events[2 * li + 1] : nullptr};
-    const EvPair *ev = events ? &pair : nullptr;
     switch (l.op) {
       case Op::SumSq:
         go(k_sumsq<Tw>, grid, block, s, ev, chunks, dyn, sumsq);
@@ -586,7 +589,8 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
       case Op::Gram:
       case Op::Poly:
       case Op::Update:
-      case Op::Last: {
+      case Op::Last:
+      case Op::GradProd: {
         GemmArgs a;
         a.tiles = tiles + l.tile_first;
         a.mats = mats;
@@ -611,10 +615,13 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
         a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
+        a.call = call;
+        a.accumulate = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
+        const bool gb = p.grad_dtype == SLORR_BF16;
         if (l.cfg == kCfg256)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev);
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev, gb);
         else
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s, ev);
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s, ev, gb);
         break;
       }
       case Op::Finalize:
@@ -638,10 +645,13 @@ void enqueue_typed(const Plan &p, hipStream_t s, hipEvent_t *events) {
 }  // namespace
 
 void enqueue(const Plan &p, hipStream_t s, hipEvent_t *events) {
-  if (p.dtype == SLORR_BF16)
-    enqueue_typed<bf16_t, _Float16>(p, s, events);
-  else
-    enqueue_typed<float, float>(p, s, events);
+  for (size_t li = 0; li < p.launches.size(); ++li) {
+    const EvPair pair{events ? events[2 * li] : nullptr, events ? events[2 * li + 1] : nullptr};
+    if (p.dtype == SLORR_BF16)
+      launch_one<bf16_t, _Float16>(p, p.launches[li], s, events ? &pair : nullptr);
+    else
+      launch_one<float, float>(p, p.launches[li], s, events ? &pair : nullptr);
+  }
 }
 
 void enqueue_apply(const Plan &p, hipStream_t s) {
@@ -663,12 +673,12 @@ void enqueue_apply(const Plan &p, hipStream_t s) {
 }
 
 void enqueue_grad(const Plan &p, hipStream_t s) {
-  if (!p.grad_launch.grid) return;
-  if (p.dtype == SLORR_BF16)
-    launch_grad<bf16_t, _Float16>(p, p.grad_launch, s, nullptr);
-  else
-    launch_grad<float, float>(p, p.grad_launch, s, nullptr);
-  check(hipGetLastError(), "kernel launch");
+  for (const Launch &l : p.grad_launches) {
+    if (p.dtype == SLORR_BF16)
+      launch_one<bf16_t, _Float16>(p, l, s, nullptr);
+    else
+      launch_one<float, float>(p, l, s, nullptr);
+  }
 }
 
 }  // namespace slorr

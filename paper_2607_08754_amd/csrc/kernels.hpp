@@ -18,8 +18,9 @@ struct HipError : std::runtime_error {
 // events[2 i + 1] after it.
 void enqueue(const Plan &p, hipStream_t s, hipEvent_t *events = nullptr);
 
-// Enqueues only the gradient kernel (p.grad_launch), reading the last iterate
-// and the gradient factors a previous enqueue left in the workspace.
+// Enqueues only the gradient launches (p.grad_launches), reading the state
+// (X_T, M, X_0) and the gradient factors a previous enqueue left in the
+// workspace.
 void enqueue_grad(const Plan &p, hipStream_t s);
 
 // Enqueues the decoupled update W <- W - s G over every matrix (one block per

@@ -42,7 +42,7 @@ struct MatDesc {
   uint64_t x0, x1, a, b;            // byte offsets in the workspace
   uint64_t c, m0, m1;               // Gram space: C = B A and the M ping-pong
   uint64_t a0;                      // Gram space: A_0 = X_0 X_0^T, kept for the trace
-  uint64_t xt;                      // buffer holding X_T once the schedule has run
+  uint64_t xt;                      // X space: buffer holding X_T once the schedule has run
 };
 
 struct DynDesc {               // per call: caller pointers

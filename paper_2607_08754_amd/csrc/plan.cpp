@@ -381,6 +381,20 @@ void build_plan(Plan &p) {
     d.chunk_end = int32_t(p.chunks.size());
   }
   p.prep.count = int32_t(p.tiles.size()) - p.prep.first;
+  // gradient tiles of the X-space matrices (the Gram-space gradient is a
+  // product, on the tiles of X_T = M X_0)
+  if (p.gs_count == 0) {
+    p.gradx = p.prep;
+  } else {
+    p.gradx.first = int32_t(p.tiles.size());
+    for (int i = 0; i < p.n; ++i) {
+      const MatDesc &d = p.mats[i];
+      if (d.empty || d.gs) continue;
+      for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
+        for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, 0));
+    }
+    p.gradx.count = int32_t(p.tiles.size()) - p.gradx.first;
+  }
 
   // workspace layout
   size_t off = 0;
@@ -406,7 +420,7 @@ void build_plan(Plan &p) {
     if (d.empty) continue;
     const size_t pq = size_t(d.Pp) * d.Qp * es, pp = size_t(d.Pp) * d.Pp * es;
     d.x0 = take(pq);
-    d.x1 = take(pq);
+    d.x1 = d.gs ? d.x0 : take(pq);            // Gram space: X_0 only (X_T is never stored)
     d.a = take(pp);
     d.b = any_quintic ? take(pp) : d.a;
     if (d.gs) {
@@ -414,7 +428,7 @@ void build_plan(Plan &p) {
       d.m0 = take(pp);
       d.m1 = take(pp);
       d.a0 = take(pp);
-      d.xt = d.x1;                            // X_T = M X_0 is written to x1
+      d.xt = d.x0;                            // unused: the gradient is a product
     } else {
       d.c = d.m0 = d.m1 = d.a0 = d.a;
       d.xt = (T & 1) ? d.x1 : d.x0;           // step t reads x[t & 1], writes the other
@@ -515,29 +529,35 @@ void build_plan(Plan &p) {
       gemm(op, p.pq, u);
     }
   }
-  // Gram space: X_T = M_{T-1} X_0 (the gradient's P; not needed for values only)
-  if (p.gs_count && !(p.flags & SLORR_VALUES_ONLY)) {
-    Launch f{};
-    f.which_x = 0;
-    f.use_m = 1;
-    f.which_m = (T - 1) & 1;
-    f.fold = 1;
-    f.alpha = float(1.0 / sm);
-    gemm(Op::Update, p.fin, f);
-  }
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
   p.launches.push_back(plain(Op::SetSum, 1));
-  p.grad_launch = Launch{};
-  if (!(p.flags & SLORR_VALUES_ONLY) && p.prep.count) {
-    Launch l = plain(Op::Grad, p.prep.count, p.prep.first);
-    p.grad_launch = l;
-    if (!(p.flags & SLORR_DEFER_GRAD)) p.launches.push_back(l);
+  // The gradient, once s1 and s2 are known: Gram space as the product
+  // X_T = M_{T-1} X_0 whose epilogue writes g (s1 X_T - s2 W) (X_T is never
+  // stored), X space by the gradient kernel from the stored X_T. A deferred
+  // gradient runs the same launches later, from the M, X_0 and X_T the
+  // forward left in the workspace.
+  p.grad_launches.clear();
+  if (!(p.flags & SLORR_VALUES_ONLY)) {
+    const size_t first = p.launches.size();
+    if (p.gs_count) {
+      Launch f{};
+      f.which_x = 0;
+      f.use_m = 1;
+      f.which_m = (T - 1) & 1;
+      f.fold = 1;
+      f.alpha = float(1.0 / sm);
+      gemm(Op::GradProd, p.fin, f);
+    }
+    if (p.gradx.count) p.launches.push_back(plain(Op::Grad, p.gradx.count, p.gradx.first));
+    p.grad_launches.assign(p.launches.begin() + first, p.launches.end());
+    if (p.flags & SLORR_DEFER_GRAD) p.launches.resize(first);
   }
 
   // MFMA work the launches execute (padded, symmetric tiles counted once)
   p.mfma_flops = 0;
   for (const Launch &l : p.launches) {
-    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last) continue;
+    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last && l.op != Op::GradProd)
+      continue;
     const double ts = tsize(l.cfg);
     for (int k = 0; k < l.grid; ++k) {
       const Tile &tl = p.tiles[l.tile_first + k];

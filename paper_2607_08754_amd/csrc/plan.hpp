@@ -26,7 +26,8 @@ enum class Op : int {
   Finalize = SLORR_OP_FINALIZE,  // values and gradient factors, one block per matrix
   Grad = SLORR_OP_GRAD,          // grad = g (s1 P - s2 W)   (original orientation)
   SetSum = SLORR_OP_SETSUM,      // set total in index order
-  GramReduce = SLORR_OP_GRAM_REDUCE   // A = sum of the split-K Gram partials
+  GramReduce = SLORR_OP_GRAM_REDUCE,  // A = sum of the split-K Gram partials
+  GradProd = SLORR_OP_GRAD_PROD  // Gram space: grad = g (s1 M X_0 - s2 W), P formed per tile
 };
 
 // GEMM block-tile configurations (kernel template instances).
@@ -86,12 +87,13 @@ struct Plan {
   int32_t gs_count = 0;                      // matrices iterated in Gram space
   double m_scale = 1.0;                      // scale of M in the iterate type
   TileRange prep;                      // prep tiles over Pp x Qp
+  TileRange gradx;                     // gradient tiles of the X-space matrices
   TileRange gsplit, gred;              // split-K Gram: part entries, reduce entries
   int32_t gram_parts = 0;              // fp32 partial tiles in the workspace
   int32_t trace_slots = 0;             // one per update tile
   std::vector<Chunk> chunks;           // original-layout element runs
   std::vector<Launch> launches;
-  Launch grad_launch{};                // the gradient epilogue (grid 0: nothing to write)
+  std::vector<Launch> grad_launches;   // the gradient (Gram-space product, X-space epilogue)
   double paper_flops = 0, mfma_flops = 0, weight_bytes = 0;
   // workspace layout (byte offsets)
   size_t off_mats = 0, off_dyn = 0, off_call = 0, off_tiles = 0, off_chunks = 0, off_scal = 0,
@@ -106,7 +108,8 @@ struct Plan {
   void *staging_event[2] = {nullptr, nullptr};
   int staging_next = 0;
   bool dyn_valid = false;
-  bool state_ready = false;    // a forward run left X_T and s1, s2 in the workspace
+  bool state_ready = false;    // a forward run left X_T (X space), M and X_0 (Gram
+                               // space) and s1, s2 in the workspace
   std::vector<DynDesc> dyn_cache;
   CallParams call_cache{};
 

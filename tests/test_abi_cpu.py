@@ -160,9 +160,11 @@ def test_plan_launch_work(L):
         te = (ctypes.c_int32 * nl)()
         assert lib.slorr_plan_get_launches(h, ops, fl, te) == L.OK
         names = [L.OPS[o] for o in ops]
-        gemm = ("gram", "poly", "update", "last")
+        gemm = ("gram", "poly", "update", "last", "grad_prod")
         assert all((e in (128, 256)) if o in gemm else e == 0 for o, e in zip(names, te))
-        assert names[:3] == ["sumsq", "norm", "prep"] and names[-3:] == ["finalize", "setsum", "grad"]
+        ngs = sum(_pad(max(s)) >= 2 * _pad(min(s)) for s in cfg.shapes)
+        tail = ["finalize", "setsum"] + ["grad_prod"] * (ngs > 0) + ["grad"] * (ngs < cfg.n)
+        assert names[:3] == ["sumsq", "norm", "prep"] and names[-len(tail):] == tail
         T = info.iters                                     # the default options: T = 6
         want = 0.0
         for m, n in cfg.shapes:
@@ -424,10 +426,12 @@ def test_split_k_gram_plan(L):
     assert info.gram_space == 3
     # first step: gram parts, reduce, poly, C = B A; later steps: A = B C, poly,
     # one update launch with M = B M_prev and C = B A (no C in the last step);
-    # then X_T = M X_0
-    assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 1 + 3
+    # finalize, set sum, then the gradient as the product X_T = M X_0 (no
+    # gradient kernel: no X-space matrix)
+    assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 3
     assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T)[0], rel=1e-12)
     # no split: per step A, poly, one update launch (B X, B M, B A); the last
-    # step's X-space update (with the trace against W) is a launch of its own
+    # step's X-space update (with the trace against W) is a launch of its own;
+    # finalize, set sum, the Gram-space gradient product, the X-space gradient
     big = facts(CONFIGS["vit_b16"].shapes)
-    assert big.launches == 3 + 3 * 6 + 1 + 1 + 3
+    assert big.launches == 3 + 3 * 6 + 1 + 4
