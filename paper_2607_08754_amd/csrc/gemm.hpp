@@ -538,8 +538,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   T *Sym = MODE == kGram ? Am : (MODE == kPoly ? Bm : Cm);
   const bool store_m0 = MODE == kPoly && tile.op == kOpPoly && args.store_m && d.gs;
   const bool store_a0 = MODE == kGram && tile.op == kOpXX && args.store_a0 && d.gs;
-  // the last M = B M_prev of a Gram-space matrix: trace partials against A_0
-  const bool mtrace = MODE == kUpdate && tile.op == kOpBM && args.trace_m;
+  // the last M = B M_prev of a Gram-space matrix (in the last step's launch,
+  // beside the X-space last updates): trace partials against A_0
+  const bool mtrace = MODE == kLast && tile.op == kOpBM && args.trace_m;
+  // an X-space last update: P and its trace against W
+  const bool xlast = MODE == kLast && tile.op == kOpBX;
   // Symmetric outputs are stored exactly symmetric: off-diagonal tiles also
   // store their transpose; a diagonal tile stores its upper triangle and the
   // transpose of it below the diagonal (its own lower triangle, computed with
@@ -549,7 +552,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const bool mirror = ((MODE == kGram || MODE == kPoly) && !part) || (MODE == kUpdate && tile.op == kOpBA);
   const bool dtile = mirror && tile.tm == tile.tn;
   constexpr bool WR = MODE == kLast || GR;    // the epilogue reads W
-  const bool colwise = mirror || (MODE == kLast && d.tall);
+  const bool colwise = mirror || (xlast && d.tall);
   double tsum = 0.0;
   const Tw *W = WR ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
 
@@ -597,11 +600,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wpre[b][t].get(j));
     return s;
   };
-  if constexpr (WR) wprefetch(0, 0);
+  if constexpr (WR)
+    if (MODE != kLast || xlast) wprefetch(0, 0);
   // Poly: the A values of the b A term, likewise one 32-row block ahead; the
   // last M product of a Gram-space matrix: the A_0 values of its trace
   XChunk<T> apre[2][NTASK];
-  const bool apref = MODE == kPoly || mtrace;
+  // (fp32 iterate: the last step's launch, which also prefetches W for its
+  // X-space tiles, reads A_0 when it uses it: registers)
+  const bool apref = MODE == kPoly || (mtrace && sizeof(T) == 2);
   const T *asrc = mtrace ? reinterpret_cast<const T *>(args.ws + d.a0) : Am;
   auto aprefetch = [&](int i, int b) {
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
@@ -611,14 +617,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       apre[b][t].load(asrc + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
     }
   };
-  if constexpr (MODE == kPoly || MODE == kUpdate)
+  if constexpr (MODE == kPoly || MODE == kLast)
     if (apref) aprefetch(0, 0);
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     if constexpr (WR)
-      if (i + 1 < FM) wprefetch(i + 1, (i + 1) & 1);
-    if constexpr (MODE == kPoly || MODE == kUpdate)
+      if (i + 1 < FM && (MODE != kLast || xlast)) wprefetch(i + 1, (i + 1) & 1);
+    if constexpr (MODE == kPoly || MODE == kLast)
       if (i + 1 < FM && apref) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
@@ -715,18 +721,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
         }
-        if (MODE == kUpdate && tile.op == kOpBM) {
+        if ((MODE == kUpdate || MODE == kLast) && tile.op == kOpBM) {
           store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
           if (mtrace) {
+            if constexpr (sizeof(T) == 2) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(apre[i & 1][t].get(j));
+              for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(apre[i & 1][t].get(j));
+            } else {
+              XChunk<T> a0;
+              a0.load(asrc + size_t(grow) * d.Pp + gcol);
+#pragma unroll
+              for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(a0.get(j));
+            }
           }
         } else if (MODE == kUpdate && tile.op == kOpBA) {
           store8_range(Cm + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
         } else if (MODE == kUpdate || (MODE == kLast && args.write_x)) {
           store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         }
-        if (MODE == kLast) {
+        if (xlast) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
           if (!d.tall) tsum += wdot(i, i & 1, t, v);

@@ -354,15 +354,19 @@ void build_plan(Plan &p) {
         fs.push_back({i, kOpBX, d.Qp, false});
       } else {
         xs.push_back({i, kOpBX, d.Qp, false});
+        ms.push_back({i, kOpBX, d.Qp, false});
         first.push_back({i, kOpBX, d.Qp, false});
         mix.push_back({i, kOpBX, d.Qp, false});
       }
     }
     // P x P products (K = Pp) take the 256-tile from one per CU (measured on
     // ViT-B/16: 432 tiles of 256 beat 1728 of 128)
-    full_list(xs, true, kMinBigTiles, p.pq);
+    // trace slots: on the X-space updates (their last one writes the
+    // partials) or, with Gram-space matrices, on the last step's launch
+    for (int c = 0; c < kNumCfg; ++c) p.pq[c] = p.plast[c] = TileRange{};
+    if (p.gs_count == 0) full_list(xs, true, kMinBigTiles, p.pq);
     full_list(first, false, kCus, p.pqc);
-    full_list(ms, true, kCus, p.mprod);
+    if (p.gs_count) full_list(ms, true, kCus, p.plast);
     full_list(fs, false, kMinBigTiles, p.fin);
     full_list(mix, false, kCus, p.pqm);
   }
@@ -511,13 +515,13 @@ void build_plan(Plan &p) {
       } else if (t < T - 1) {
         gemm(Op::Update, p.pqm, u);
       } else {
-        gemm(Op::Last, p.pq, u);
-        // the last M writes the trace partials: with X_T = M X_0 and
-        // X_0 = Y / (f + eps), sum(W * P) = (f + eps) tr(X_0^T M X_0) =
-        // (f + eps) tr(M A_0)
+        // one launch: the X-space last updates (trace against W) and the
+        // last M of the Gram-space matrices, whose trace partials follow from
+        // X_T = M X_0 and X_0 = W / (f + eps): sum(W * P) =
+        // (f + eps) tr(X_0^T M X_0) = (f + eps) tr(M A_0)
         u.trace_m = 1;
         u.tscale = float(1.0 / (sm * double(sa)));
-        gemm(Op::Update, p.mprod, u);
+        gemm(Op::Last, p.plast, u);
       }
     } else {
       // cubic step (no Gram-space matrices): X'_s = a X_s + b (A_s X_s) / s_a

@@ -82,7 +82,8 @@ struct Plan {
   TileRange pq[kNumCfg];                     // P x Q outputs (update, last) of X-space matrices
   TileRange pqc[kNumCfg];                    // first step: X-space updates and Gram-space C = B A
   TileRange pqm[kNumCfg];                    // later steps: also Gram-space M = B M_prev
-  TileRange mprod[kNumCfg];                  // Gram space: the last M = B M_prev
+  TileRange plast[kNumCfg];                  // Gram-space sets, last step: X-space B X and
+                                             // Gram-space M = B M_prev, both with trace partials
   TileRange fin[kNumCfg];                    // Gram space: X_T = M X_0
   int32_t gs_count = 0;                      // matrices iterated in Gram space
   double m_scale = 1.0;                      // scale of M in the iterate type

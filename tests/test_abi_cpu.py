@@ -430,8 +430,8 @@ def test_split_k_gram_plan(L):
     # gradient kernel: no X-space matrix)
     assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 3
     assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T)[0], rel=1e-12)
-    # no split: per step A, poly, one update launch (B X, B M, B A); the last
-    # step's X-space update (with the trace against W) is a launch of its own;
-    # finalize, set sum, the Gram-space gradient product, the X-space gradient
+    # no split: per step A, poly, one update launch (B X, B M, B A; the last
+    # step's with the trace partials of both kinds); finalize, set sum, the
+    # Gram-space gradient product, the X-space gradient
     big = facts(CONFIGS["vit_b16"].shapes)
-    assert big.launches == 3 + 3 * 6 + 1 + 4
+    assert big.launches == 3 + 3 * 6 + 4
