@@ -164,7 +164,8 @@ __device__ __forceinline__ void lds_dma_wait() {
 // sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
 // Gradient run of nv elements at g: u = fl(gsc fl(s1 p - s2 w)) (u rounded to
 // bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
-// contraction, the rounding the gradient kernel uses.
+// contraction, the rounding the gradient kernel uses. Whole runs are stored
+// non-temporally (the gradient is not read again in the call).
 template <typename Tg>
 __device__ __forceinline__ void grad8(Tg *g, int nv, const float (&p)[8], const float (&w)[8], float s1,
                                       float s2, float gsc, int accumulate) {
@@ -182,7 +183,26 @@ __device__ __forceinline__ void grad8(Tg *g, int nv, const float (&p)[8], const 
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = old[j] + v[j];
   }
-  put8(g, nv, v);
+  if (nv == 8 && (reinterpret_cast<uintptr_t>(g) & 15) == 0) {
+    if constexpr (sizeof(Tg) == 2) {
+      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+      u16x8 h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) h[j] = from_f<Tg>(v[j]);
+      __builtin_nontemporal_store(h, reinterpret_cast<u16x8 *>(g));
+    } else {
+      float4v a, b;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[j] = v[j];
+        b[j] = v[4 + j];
+      }
+      __builtin_nontemporal_store(a, reinterpret_cast<float4v *>(g));
+      __builtin_nontemporal_store(b, reinterpret_cast<float4v *>(g) + 1);
+    }
+  } else {
+    put8(g, nv, v);
+  }
 }
 
 template <typename Tw>
