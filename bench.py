@@ -36,21 +36,25 @@ def kernel_instance(op, edge):
     return f"k_gemm<{KERNEL_MODE[op]}, {edge}x{edge}>"
 
 
-def _alg_bytes_per_launch(shapes, dtype, op):
+def _alg_bytes_per_launch(shapes, dtype, op, gram_space):
     """Bytes the memory-bound kernels must move: sumsq reads W (a2); prep reads W
-    and writes X_0 (a3); grad reads W and P and writes the fp32 gradient (a7)."""
+    and writes X_0 (a3); grad reads W and P and writes the fp32 gradient (a7)
+    of the matrices iterated in X space (a Gram-space matrix's gradient is
+    written by its last product)."""
     wb = 2 if dtype == "bf16" else 4          # weight element
     xb = 2 if dtype == "bf16" else 4          # iterate element (fp16 / fp32)
+    pad = lambda x: (x + 127) // 128 * 128
     tot = 0
     for m, n in shapes:
         e = m * n
-        tot += {"sumsq": wb * e, "prep": (wb + xb) * e, "grad": (wb + xb + 4) * e}[op]
+        gs = gram_space and pad(max(m, n)) >= 2 * pad(min(m, n))
+        tot += {"sumsq": wb * e, "prep": (wb + xb) * e, "grad": 0 if gs else (wb + xb + 4) * e}[op]
     return float(tot)
 
 
 def integration_timings(cfg, kind, W, G, steps):
     """The training-loop routes on the same set (one GPU): the autograd route
-    (forward with the gradient deferred, then the gradient kernel with the
+    (forward with the gradient deferred, then the gradient launches with the
     upstream factors read on the device), the accumulate route (App. E.3,
     one call with grad += lambda G) and the decoupled update kernel
     (App. E.2, W <- W - s G_pre, timed on a copy of the weights)."""
@@ -334,7 +338,7 @@ def main():
     hbm = {}
     for op in ("sumsq", "prep", "grad"):
         if op in op_ms:
-            b = _alg_bytes_per_launch(cfg.shapes, cfg.dtype, op)
+            b = _alg_bytes_per_launch(cfg.shapes, cfg.dtype, op, info["gram_space"] > 0)
             hbm[op] = {"alg_bytes": b, "avg_ms": op_ms[op]["avg_ms"],
                        "GB/s": round(b / (op_ms[op]["avg_ms"] * 1e-3) / 1e9, 1)}
 
