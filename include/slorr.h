@@ -85,8 +85,8 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
 #define SLORR_VALUES_ONLY 0x2u  /* values only: no gradient is written, out_grads may be NULL */
 #define SLORR_NO_GRAPH    0x4u  /* enqueue kernels one by one instead of replaying a hipGraph */
 #define SLORR_AUX         0x8u  /* out_vals also receives n_hat_i and f_i (see below) */
-#define SLORR_DEFER_GRAD  0x10u /* slorr_reg_fwd_bwd computes the values and keeps the last
-                                   iterate and the gradient factors in the workspace; the
+#define SLORR_DEFER_GRAD  0x10u /* slorr_reg_fwd_bwd computes the values and keeps the
+                                   iterate state and the gradient factors in the workspace; the
                                    gradient is written later by slorr_reg_grad (autograd
                                    backward, Listing 1). out_grads may be NULL. */
 
@@ -166,8 +166,10 @@ SLORR_API slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const v
                                  void *stream);
 
 /* Gradient from the state a preceding slorr_reg_fwd_bwd on this plan left in
- * the workspace (the last iterate P and the factors s1, s2): the backward half
- * of a forward run with SLORR_DEFER_GRAD (or any run that wrote gradients).
+ * the workspace (the last iterate P of X-space matrices, M_{T-1} and X_0 of
+ * Gram-space ones, and the factors s1, s2): the backward half of a forward
+ * run with SLORR_DEFER_GRAD (or any run that wrote gradients). It runs the
+ * same gradient launches as the one-call path.
  *   n, weights, shapes, kind, iters : as in that call; weights must hold the
  *               same values (the Hoyer gradient reads W again).
  *   out_grads : as in slorr_reg_fwd_bwd (grad_dtype, alignment, no overlap),
