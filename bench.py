@@ -170,7 +170,7 @@ SWEEPS = {
 }
 
 
-def run_sweep(which, kind, steps, warmup):
+def run_sweep(which, kind, steps, warmup, x_space=False):
     """Weight-sets/s of each set of a sweep (graph replay, inputs resident);
     one JSON line with a row per set."""
     import numpy as np
@@ -187,7 +187,7 @@ def run_sweep(which, kind, steps, warmup):
               else torch.from_numpy(a)).to(dev) for a in arrs]
         del arrs
         G = [torch.empty(w.shape, dtype=torch.float32, device=dev) for w in W]
-        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, device=dev)
+        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, x_space=x_space, device=dev)
         for _ in range(warmup):
             plan(W, G)
         torch.cuda.synchronize()
@@ -233,6 +233,8 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
+    ap.add_argument("--x-space", action="store_true",
+                    help="iterate every matrix in X space (the paper's form), for comparison")
     ap.add_argument("--sweep", choices=["vit", "llm", "configs", "all"], default=None,
                     help="time every set of a sweep (App. D ViT configurations, App. F LLM shapes, "
                          "or the five configured sets) instead of the headline workload; prints one "
@@ -249,7 +251,7 @@ def main():
     from workloads import CONFIGS, make_set
 
     if args.sweep:
-        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)))
+        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)), args.x_space)
         return
 
     if args.calibrate_copy:
@@ -271,7 +273,7 @@ def main():
         t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if cfg.dtype == "bf16" else torch.from_numpy(a)
         W.append(t.to(dev))
     G = [torch.empty(a.shape, dtype=torch.float32, device=dev) for a in arrs]
-    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, device=dev)
+    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, x_space=args.x_space, device=dev)
     info = plan.info()
     print(f"[bench] {cfg.name}: {cfg.n} matrices, inputs ready in {time.perf_counter() - t_gen:.1f} s, "
           f"{info['launches']} launches per step", file=sys.stderr, flush=True)

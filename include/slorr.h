@@ -89,6 +89,9 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
                                    iterate state and the gradient factors in the workspace; the
                                    gradient is written later by slorr_reg_grad (autograd
                                    backward, Listing 1). out_grads may be NULL. */
+#define SLORR_X_SPACE     0x20u /* iterate every matrix in X space (X <- a X + (b A + c A^2) X,
+                                   the paper's form, Sec. 3) instead of Gram space for the
+                                   wide ones (more work, the paper's rounding order) */
 
 typedef struct {
   int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */

@@ -161,7 +161,6 @@ __device__ __forceinline__ void lds_dma_wait() {
 #endif
 }
 
-// sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
 // Gradient run of nv elements at g: u = fl(gsc fl(s1 p - s2 w)) (u rounded to
 // bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
 // contraction, the rounding the gradient kernel uses. Whole runs are stored
@@ -205,6 +204,7 @@ __device__ __forceinline__ void grad8(Tg *g, int nv, const float (&p)[8], const 
   }
 }
 
+// sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
 template <typename Tw>
 __device__ __forceinline__ double dot_w(const Tw *w, const float (&v)[8], int n) {
   float wv[8];

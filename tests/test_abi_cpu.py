@@ -115,6 +115,13 @@ def _expected_mfma(shapes, T):
     return tot, sum(gs)
 
 
+def _expected_mfma_x(shapes, T):
+    """MFMA work of an all-X-space schedule (no split-K): per step A = X X^T and
+    the poly on upper-triangle 128-tiles, B X on all tiles."""
+    mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
+    return T * sum(2 * _tri(P, 128) * Q + 2 * _tri(P, 128) * P + 2.0 * P * P * Q for P, Q in mats)
+
+
 @pytest.mark.parametrize("name", list(CONFIGS))
 def test_plan_facts(L, name):
     cfg = CONFIGS[name]
@@ -194,6 +201,14 @@ def test_plan_gram_space_selection(L):
     assert info.m_scale > 0 and math.log2(info.m_scale) == int(math.log2(info.m_scale))
     L.lib().slorr_plan_destroy(h)
     opts = L.Options()
+    L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.flags = L.X_SPACE                                 # the paper's form, asked for
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
+    assert st == L.OK
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 0
+    assert info.mfma_flops == pytest.approx(_expected_mfma_x(shapes, info.iters), rel=1e-12)
+    L.lib().slorr_plan_destroy(h)
     L.lib().slorr_default_options(ctypes.byref(opts))
     opts.degree = 3
     st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)

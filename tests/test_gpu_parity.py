@@ -103,6 +103,19 @@ def test_gram_space_schedules(dtype, iters):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_x_space_flag(dtype):
+    """x_space=True keeps the wide matrices in X space (the paper's form): the
+    matrices of the Gram-space test, both kinds, against the oracle."""
+    shapes = [(96, 300), (300, 96), (128, 512), (250, 260)]
+    arrs = [gaussian(s, seed=23, std=0.05, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+    for kind in ("hoyer", "nuclear"):
+        vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=1e-4, g=0.8, x_space=True)
+        assert plan.info()["gram_space"] == 0
+        refs = run_oracle(arrs, dtype, kind, 6, eps=1e-4, g=0.8)
+        compare(vals, grads, refs, kind, dtype, g=0.8, label=f"x space {dtype} {kind}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_split_k_gram_long_rows(dtype):
     """Few Gram tiles with long k ranges: the split-K Gram (parts of unequal
     length when Qp / 128 is not a multiple of the part count) and its reduce."""
