@@ -161,19 +161,17 @@ __device__ __forceinline__ void lds_dma_wait() {
 #endif
 }
 
-// Gradient run of nv elements at g: u = fl(gsc fl(s1 p - s2 w)) (u rounded to
-// bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
+// Gradient run of nv elements at g from t = s1 P - s2 W: u = fl(gsc t) (u
+// rounded to bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
 // contraction, the rounding the gradient kernel uses. Whole runs are stored
 // non-temporally (the gradient is not read again in the call).
 template <typename Tg>
-__device__ __forceinline__ void grad8(Tg *g, int nv, const float (&p)[8], const float (&w)[8], float s1,
-                                      float s2, float gsc, int accumulate) {
+__device__ __forceinline__ void grad8(Tg *g, int nv, const float (&t)[8], float gsc, int accumulate) {
 #pragma clang fp contract(off)
   float v[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const float t = s1 * p[j] - s2 * w[j];
-    v[j] = gsc * t;
+    v[j] = gsc * t[j];
     if constexpr (sizeof(Tg) == 2) v[j] = to_f(from_f<Tg>(v[j]));
   }
   if (accumulate) {
@@ -523,6 +521,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // K is a multiple of 128 (padding) and BK divides it. One LDS stage is
   // multiplied while the other is filled by direct loads (and the transposed
   // update operand) for the next slab.
+  // Grad: the product runs on M - r I, r = s2 (f + eps) / s1, so that it
+  // gives s1 (M - r I) X_0 = s1 P - s2 W (W = (f + eps) X_0) and the epilogue
+  // reads no W: where a k-slab crosses the tile's rows, the diagonal entries
+  // of M in the published LDS stage are shifted (then a barrier) before the
+  // slab's MFMAs read them.
+  float shift = 0.0f;
+  if constexpr (GR) {
+    const Scalars sv = args.sc[tile.mat];
+    if (sv.s1 != 0.0) shift = float(sv.s2 * sv.feps / sv.s1 * double(args.mscale));
+  }
+  auto dshift = [&](int kt, int buf) {
+    if constexpr (GR) {
+      const int k0 = kt * BK, lo = max(k0, m0), hi = min(k0 + BK, m0 + BM);
+      if (shift != 0.0f && lo < hi) {              // uniform over the block
+        if (tid < hi - lo) {
+          const int m = lo + tid, r = m - m0, kk = m - k0;
+          T *e = reinterpret_cast<T *>(smem + buf * S::kStage + swz(r, kk / V)) + kk % V;
+          *e = T(float(*e) - shift);
+        }
+        __syncthreads();
+      }
+    }
+  };
   const int nk = K / BK;
   dload(0, 0);
   kload(0);
@@ -535,6 +556,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       dload((kt + 1) * BK, nb);
       kload((kt + 1) * BK);
     }
+    dshift(kt, kt & 1);
     compute(kt & 1);
     if (kt + 1 < nk) kstore(nb);
     lds_dma_wait();
@@ -571,7 +593,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // B Y drift apart over the steps.
   const bool mirror = ((MODE == kGram || MODE == kPoly) && !part) || (MODE == kUpdate && tile.op == kOpBA);
   const bool dtile = mirror && tile.tm == tile.tn;
-  constexpr bool WR = MODE == kLast || GR;    // the epilogue reads W
+  constexpr bool WR = MODE == kLast || GR;    // the epilogue reads W or writes in its layout
   const bool colwise = mirror || (xlast && d.tall);
   double tsum = 0.0;
   const Tw *W = WR ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
@@ -620,8 +642,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wpre[b][t].get(j));
     return s;
   };
-  if constexpr (WR)
-    if (MODE != kLast || xlast) wprefetch(0, 0);
+  if constexpr (MODE == kLast)
+    if (xlast) wprefetch(0, 0);
   // Poly: the A values of the b A term, likewise one 32-row block ahead; the
   // last M product of a Gram-space matrix: the A_0 values of its trace
   XChunk<T> apre[2][NTASK];
@@ -642,8 +664,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
-    if constexpr (WR)
-      if (i + 1 < FM && (MODE != kLast || xlast)) wprefetch(i + 1, (i + 1) & 1);
+    if constexpr (MODE == kLast)
+      if (i + 1 < FM && xlast) wprefetch(i + 1, (i + 1) & 1);
     if constexpr (MODE == kPoly || MODE == kLast)
       if (i + 1 < FM && apref) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
@@ -655,12 +677,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     __builtin_amdgcn_wave_barrier();
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
     if constexpr (GR) {
-      // g (s1 P - s2 W) straight from the staged block, in W's orientation:
-      // runs of 8 along W's rows (canonical rows of a wide W, canonical
-      // columns of a tall one), the tasks wtask and the W prefetch use
+      // g s1 (P - r X_0) = g (s1 P - s2 W) straight from the staged block, in
+      // W's orientation: runs of 8 along W's rows (canonical rows of a wide W,
+      // canonical columns of a tall one), the tasks of wtask
       typedef typename std::conditional<MODE == kGradB, bf16_t, float>::type Tg;
       Tg *G = static_cast<Tg *>(args.dyn[tile.mat].g);
-      const float s1 = float(args.sc[tile.mat].s1) * args.inv_sx, s2 = float(args.sc[tile.mat].s2);
+      const float s1 = float(args.sc[tile.mat].s1) * args.inv_sx;
       const float gsc = args.call->gscale ? args.call->grad_scale * args.call->gscale[tile.mat]
                                           : args.call->grad_scale;
 #pragma unroll
@@ -669,7 +691,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         const Tw *ptr;
         int nv;
         if (!wtask(i, t, ptr, nv)) continue;
-        float v[8], wv[8];
+        float v[8];
         if (!d.tall) {
           const float4v *e = reinterpret_cast<const float4v *>(ep + (task / CG) * P + (task % CG) * 8);
           const float4v e0 = e[0], e1 = e[1];
@@ -682,13 +704,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = ep[((task & 3) * 8 + j) * P + (task >> 2)] * alpha;
         }
-        if (wfull[i & 1][t]) {
+        float tv[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) wv[j] = wpre[i & 1][t].get(j);
-        } else {
-          get8(ptr, nv, wv);
-        }
-        grad8(G + (ptr - W), nv, v, wv, s1, s2, gsc, args.accumulate);
+        for (int j = 0; j < 8; ++j) tv[j] = s1 * v[j];
+        grad8(G + (ptr - W), nv, tv, gsc, args.accumulate);
       }
       __builtin_amdgcn_wave_barrier();
       continue;

@@ -537,8 +537,9 @@ void build_plan(Plan &p) {
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
   p.launches.push_back(plain(Op::SetSum, 1));
   // The gradient, once s1 and s2 are known: Gram space as the product
-  // X_T = M_{T-1} X_0 whose epilogue writes g (s1 X_T - s2 W) (X_T is never
-  // stored), X space by the gradient kernel from the stored X_T. A deferred
+  // s1 (M_{T-1} - r I) X_0 = s1 X_T - s2 W (r = s2 (f + eps) / s1, W =
+  // (f + eps) X_0) whose epilogue writes g times it (X_T is never stored),
+  // X space by the gradient kernel from the stored X_T. A deferred
   // gradient runs the same launches later, from the M, X_0 and X_T the
   // forward left in the workspace.
   p.grad_launches.clear();
@@ -551,6 +552,7 @@ void build_plan(Plan &p) {
       f.which_m = (T - 1) & 1;
       f.fold = 1;
       f.alpha = float(1.0 / sm);
+      f.mscale = float(sm);            // the scale of M: the shift r I is applied at it
       gemm(Op::GradProd, p.fin, f);
     }
     if (p.gradx.count) p.launches.push_back(plain(Op::Grad, p.gradx.count, p.gradx.first));
