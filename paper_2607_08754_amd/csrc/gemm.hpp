@@ -72,7 +72,8 @@ struct GemmArgs {
   int use_a;      // update operand is A (cubic step)
   int use_m;      // update operand is M (Gram space: X_T = M X_0)
   int which_m;    // M buffer: written by a B M product, read by X_T = M X_0
-  int store_m;    // poly: also store M_0 = B, scaled by mscale, for Gram-space matrices
+  int which_b;    // B buffer: b (0) or b1 (1)
+  int m_from_b;   // M = B M_prev reads M_prev = B_0 from b
   int store_a0;   // first Gram: also store A_0 for Gram-space matrices
   int trace_m;    // M = B M_prev: per-tile partials of (f + eps) tr(M A_0) * tscale
   float tscale;
@@ -80,8 +81,8 @@ struct GemmArgs {
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
   float alpha, beta, gamma, inv_sx;
-  float alpha2;   // scale of the Gram-space A = B C
-  float mscale;
+  float alpha2;   // scale of the Gram-space A = B C and M = B M_prev
+  float mscale;   // gradient product: scale of M
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
   const CallParams *call;   // Grad: upstream factors
   int accumulate; // Grad: add into the gradient buffers
@@ -370,10 +371,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
   T *Xn = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x0 : d.x1));
   T *Am = reinterpret_cast<T *>(args.ws + d.a);
-  T *Bm = reinterpret_cast<T *>(args.ws + d.b);
+  T *Bm = reinterpret_cast<T *>(args.ws + (args.which_b ? d.b1 : d.b));
   T *Cm = reinterpret_cast<T *>(args.ws + d.c);
   T *Mw = reinterpret_cast<T *>(args.ws + (args.which_m ? d.m1 : d.m0));   // M written / read
-  T *Mr = reinterpret_cast<T *>(args.ws + (args.which_m ? d.m0 : d.m1));   // M_prev of B M
+  T *Mr = reinterpret_cast<T *>(args.ws + (args.m_from_b ? d.b : args.which_m ? d.m0 : d.m1));   // M_prev of B M
 
   const T *Ap;
   const T *Bp;
@@ -572,13 +573,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
-  // Gram-space A = B C scales by alpha2; the poly adds b A + a I
-  const bool gsp = MODE == kGram && tile.op == kOpBC;
+  // Gram-space A = B C and M = B M_prev scale by alpha2; the poly adds b A + a I
+  const bool gsp = (MODE == kGram && tile.op == kOpBC) || (KN && tile.op == kOpBM);
   const float alpha = gsp ? args.alpha2 : args.alpha, beta = args.beta;
-  // symmetric output and where it goes; the first poly of a Gram-space matrix
-  // also stores M_0 = B (scaled)
+  // symmetric output and where it goes
   T *Sym = MODE == kGram ? Am : (MODE == kPoly ? Bm : Cm);
-  const bool store_m0 = MODE == kPoly && tile.op == kOpPoly && args.store_m && d.gs;
   const bool store_a0 = MODE == kGram && tile.op == kOpXX && args.store_a0 && d.gs;
   // the last M = B M_prev of a Gram-space matrix (in the last step's launch,
   // beside the X-space last updates): trace partials against A_0
@@ -744,12 +743,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
           v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
         const int lo = dtile ? grow - gcol : 0;
         store8_range(Sym + size_t(grow) * d.Pp + gcol, v, lo, 8);
-        if (store_m0) {
-          float mv[8];
-#pragma unroll
-          for (int j = 0; j < 8; ++j) mv[j] = v[j] * args.mscale;
-          store8_range(reinterpret_cast<T *>(args.ws + d.m0) + size_t(grow) * d.Pp + gcol, mv, lo, 8);
-        }
       } else {
         if (args.fold) {
 #pragma unroll
@@ -810,11 +803,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
           const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
           store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
           if (store_a0) store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(orow) * d.Pp + ocol, v, 0, hi);
-          if (store_m0) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) v[j] *= args.mscale;
-            store8_range(reinterpret_cast<T *>(args.ws + d.m0) + size_t(orow) * d.Pp + ocol, v, 0, hi);
-          }
         } else if (MODE == kLast) {
           tsum += wdot(i, i & 1, t, v);       // tall W (colwise only for tall)
         }

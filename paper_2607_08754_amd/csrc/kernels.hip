@@ -601,7 +601,8 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev)
         a.use_a = l.use_a;
         a.use_m = l.use_m;
         a.which_m = l.which_m;
-        a.store_m = l.store_m;
+        a.which_b = l.which_b;
+        a.m_from_b = l.m_from_b;
         a.write_x = (p.flags & SLORR_VALUES_ONLY) ? 0 : 1;
         a.alpha = l.alpha;
         a.beta = l.beta;

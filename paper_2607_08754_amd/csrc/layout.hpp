@@ -41,6 +41,7 @@ struct MatDesc {
   int32_t pad;
   uint64_t x0, x1, a, b;            // byte offsets in the workspace
   uint64_t c, m0, m1;               // Gram space: C = B A and the M ping-pong
+  uint64_t b1;                      // Gram space: B of odd steps (B of even steps at b)
   uint64_t a0;                      // Gram space: A_0 = X_0 X_0^T, kept for the trace
   uint64_t xt;                      // X space: buffer holding X_T once the schedule has run
 };

@@ -429,12 +429,14 @@ void build_plan(Plan &p) {
     d.a = take(pp);
     d.b = any_quintic ? take(pp) : d.a;
     if (d.gs) {
+      d.b1 = take(pp);
       d.c = take(pp);
       d.m0 = take(pp);
       d.m1 = take(pp);
       d.a0 = take(pp);
       d.xt = d.x0;                            // unused: the gradient is a product
     } else {
+      d.b1 = d.b;
       d.c = d.m0 = d.m1 = d.a0 = d.a;
       d.xt = (T & 1) ? d.x1 : d.x0;           // step t reads x[t & 1], writes the other
     }
@@ -472,6 +474,7 @@ void build_plan(Plan &p) {
     // (later steps) A = B C of the previous step
     Launch g{};
     g.which_x = wx;
+    g.which_b = (t + 1) & 1;                  // B of the previous step
     g.alpha = float(sa / (double(sx) * sx));
     g.alpha2 = prod;
     g.store_a0 = (t == 0 && p.gs_count) ? 1 : 0;
@@ -491,23 +494,26 @@ void build_plan(Plan &p) {
     const Op op = (t == T - 1) ? Op::Last : Op::Update;
     if (quintic) {
       // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
-      // the step X' = a X + (b A + c A A) X becomes X' = B X. The first poly
-      // also stores M_0 = B for the Gram-space matrices, at M's scale.
+      // the step X' = a X + (b A + c A A) X becomes X' = B X. Gram-space
+      // matrices keep B_t in b[t & 1], so that B_0 serves as M_0.
       Launch l{};
       l.which_x = wx;
+      l.which_b = t & 1;
       l.alpha = float(double(sb) * c / (double(sa) * sa));
       l.beta = float(double(sb) * b / sa);
       l.gamma = float(double(sb) * a);
-      l.store_m = (t == 0 && p.gs_count) ? 1 : 0;
-      l.mscale = float(sm / sb);
       gemm(Op::Poly, p.pp, l);
-      // X'_s = (B_s X_s) / s_b; Gram space (after the first step, where
-      // M_0 = B): M_t = B M_{t-1}, read from m[(t - 1) & 1], written to m[t & 1]
+      // X'_s = (B_s X_s) / s_b; Gram space: M_t = B_t M_{t-1}, written to
+      // m[t & 1], read from m[(t - 1) & 1], or, at t = 1, M_0 = B_0 read from
+      // b: (B_s M_s) / s_b, or s_m (B_s B_0s) / s_b^2 at t = 1
       Launch u{};
       u.which_x = wx;
+      u.which_b = t & 1;
       u.which_m = t & 1;
+      u.m_from_b = t == 1 ? 1 : 0;
       u.fold = 1;
       u.alpha = prod;
+      u.alpha2 = t == 1 ? float(sm / (double(sb) * sb)) : prod;
       // and C = B A for the next step's A = B C (t < T - 1)
       if (!p.gs_count) {
         gemm(op, p.pq, u);

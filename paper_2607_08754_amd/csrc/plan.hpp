@@ -46,13 +46,14 @@ struct Launch {
   int32_t use_a;       // update operand is A (cubic step) instead of B
   int32_t use_m;       // update operand is M (Gram space: X_T = M X_0)
   int32_t which_m;     // M buffer written (products) or read (X_T = M X_0)
-  int32_t store_m;     // poly: also store M_0 = B (Gram-space matrices)
+  int32_t which_b;     // B buffer of the step (Gram space: B_t in b[t & 1])
+  int32_t m_from_b;    // M = B M_prev with M_prev = B_0 (second step: M_0 = B_0 is not stored)
   int32_t store_a0;    // first Gram: also store A_0 (Gram-space matrices)
   int32_t trace_m;     // last M = B M_prev: trace partials of M A_0 (Gram space)
   int32_t fold;        // update: a_t I already folded into B (no a X term)
   float alpha, beta, gamma;  // epilogue coefficients
-  float alpha2;        // Gram-space A = B C
-  float mscale;        // poly: scale of the stored M_0 relative to B
+  float alpha2;        // Gram-space A = B C; M = B M_prev
+  float mscale;        // gradient product: scale of M
   float tscale;        // trace_m: 1 / (s_m s_a), the scales of M and A_0
 };
 
