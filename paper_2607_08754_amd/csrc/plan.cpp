@@ -361,12 +361,13 @@ void build_plan(Plan &p) {
       }
     }
     // P x P products (K = Pp) take the 256-tile from one per CU (measured on
-    // ViT-B/16: 432 tiles of 256 beat 1728 of 128)
+    // ViT-B/16: 648 tiles of 256 beat 2484 of 128), except in the first
+    // step's launch (C = B A only: 324 tiles of 256 lose to 1188 of 128)
     // trace slots: on the X-space updates (their last one writes the
     // partials) or, with Gram-space matrices, on the last step's launch
     for (int c = 0; c < kNumCfg; ++c) p.pq[c] = p.plast[c] = TileRange{};
     if (p.gs_count == 0) full_list(xs, true, kMinBigTiles, p.pq);
-    full_list(first, false, kCus, p.pqc);
+    full_list(first, false, kMinBigTiles, p.pqc);
     if (p.gs_count) full_list(ms, true, kCus, p.plast);
     full_list(fs, false, kMinBigTiles, p.fin);
     full_list(mix, false, kCus, p.pqm);

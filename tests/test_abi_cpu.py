@@ -80,8 +80,8 @@ def _expected_mfma(shapes, T):
     later A and the poly; full products (B X, M = B M_prev, X_T = M X_0) on all
     tiles. C = B A runs in the update launch of its step (with the X-space
     B X and, after the first step, M = B M_prev), whose tiles are 256 x 256
-    when all its products allow it and it has one per CU. Matrices with
-    padded Q >= 2 P iterate in Gram space."""
+    when all its products allow it and it has one per CU (two in the first
+    step). Matrices with padded Q >= 2 P iterate in Gram space."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
     gs = [Q >= 2 * P for P, Q in mats]
 
@@ -96,14 +96,14 @@ def _expected_mfma(shapes, T):
     if gps and T > 1:
         t1 = cfg(ps, 512)
         tot += (T - 1) * sum(2 * _tri(P, t1) * (P if g else Q) for (P, Q), g in zip(mats, gs))
-        def ucfg(prods):                       # (P, output columns, upper) of one update launch
+        def ucfg(prods, min_big):              # (P, output columns, upper) of one update launch
             big = sum((P // 256) * (P // 256 + 1) // 2 if up else (P // 256) * (N // 256) for P, N, up in prods)
             ok = all(P % 256 == 0 and N % 256 == 0 for P, N, _ in prods)
-            return 256 if ok and big >= 256 else 128
+            return 256 if ok and big >= min_big else 128
         sq = [(P, Q, False) for (P, Q), g in zip(mats, gs) if not g]
         c = [(P, P, True) for P in gps]
-        tc0 = ucfg(sq + c)
-        tcm = ucfg(sq + [(P, P, False) for P in gps] + c)
+        tc0 = ucfg(sq + c, 512)
+        tcm = ucfg(sq + [(P, P, False) for P in gps] + c, 256)
         tot += sum(2 * _tri(P, tc0) * P for P in gps)                   # C = B A, first step
         tot += (T - 2) * sum(2 * _tri(P, tcm) * P for P in gps)         # C = B A, later steps
         tot += (T - 1) * sum(2.0 * P ** 3 for P in gps)                  # M = B M_prev
