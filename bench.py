@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -93,14 +94,27 @@ def integration_timings(cfg, kind, W, G, steps):
     return out
 
 
-def _kernels_hash():
-    """Hash of the library's sources (kernels and the plan that orders their tiles)."""
+def _code_only(text):
+    """C++ source without comments and blank lines (what the compiler sees)."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+
+
+def _kernels_hash(read=None):
+    """Hash of the library's sources (kernels and the plan that orders their
+    tiles), comments left out: a traffic record stays valid across comment
+    edits and goes stale with any change of code."""
     csrc = os.path.join(ROOT, "paper_2607_08754_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(csrc)):
         if name.endswith((".hip", ".hpp", ".cpp", ".h")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+            if read is None:
+                with open(os.path.join(csrc, name), encoding="utf-8") as f:
+                    text = f.read()
+            else:
+                text = read(name)
+            h.update(name.encode() + b"\0" + _code_only(text).encode())
     return h.hexdigest()[:16]
 
 

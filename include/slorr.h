@@ -216,8 +216,9 @@ typedef enum {
   SLORR_OP_GRAM = 3,      /* A = X X^T; Gram space: A = B C               */
   SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
   SLORR_OP_UPDATE = 5,    /* X = a_t X + B X; Gram space: M = B M_prev,   */
-                          /* C = B A, X_T = M X_0                         */
-  SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
+                          /* C = B A                                      */
+  SLORR_OP_LAST = 6,      /* last update: P and the trace partials (Gram  */
+                          /* space: the last M, trace tr(M A_0))          */
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
   SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
@@ -253,8 +254,8 @@ typedef struct {
   double mfma_flops;       /* flops the MFMA units execute per call (padded tiles)   */
   double weight_bytes;     /* sum_i rows_i * cols_i * sizeof(dtype)                  */
   size_t workspace_bytes;
-  int32_t gram_space;      /* matrices iterated in Gram space (P x P products and    */
-                           /* X_T = M X_0; padded Q >= 2 P, quintic tables)          */
+  int32_t gram_space;      /* matrices iterated in Gram space (P x P products, the   */
+                           /* gradient from M X_0; padded Q >= 2 P, quintic tables)  */
   double m_scale;          /* scale of M in the iterate type                         */
 } slorr_plan_info_t;
 
@@ -265,7 +266,8 @@ SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_
  * kernel kind (slorr_op_t) of launch i; alg_flops[i] its algorithmic work:
  * the products it performs, on the unpadded shapes and counted in full
  * (2 m n k each, symmetric outputs not halved): A = X X^T 2 P^2 Q, B X and
- * X_T = M X_0 2 P^2 Q, every P x P product (poly, Gram space) 2 P^3; 0 for
+ * the gradient product M X_0 2 P^2 Q, every P x P product (poly, Gram
+ * space) 2 P^3; 0 for
  * the memory-bound and reduction kernels. tile_edge[i] is the block tile edge
  * of a product launch (128 or 256: the kernel instance a profiler names), 0
  * for the others. Any of the three arrays may be NULL. Host only. */

@@ -70,8 +70,8 @@ struct GemmArgs {
   double *tpart;
   int which_x;    // current X buffer
   int use_a;      // update operand is A (cubic step)
-  int use_m;      // update operand is M (Gram space: X_T = M X_0)
-  int which_m;    // M buffer: written by a B M product, read by X_T = M X_0
+  int use_m;      // the A operand is M (Gram-space gradient product M X_0)
+  int which_m;    // M buffer: written by a B M product, read by M X_0
   int which_b;    // B buffer: b (0) or b1 (1)
   int m_from_b;   // M = B M_prev reads M_prev = B_0 from b
   int store_a0;   // first Gram: also store A_0 for Gram-space matrices

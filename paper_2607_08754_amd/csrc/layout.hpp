@@ -37,7 +37,7 @@ struct MatDesc {
   int32_t empty;               // rows == 0 or cols == 0
   int32_t chunk_begin, chunk_end;   // slots in the norm-partials array
   int32_t trace_begin, trace_end;   // slots in the trace-partials array
-  int32_t gs;                  // iterated in Gram space (P x P products, X_T = M X_0)
+  int32_t gs;                  // iterated in Gram space (P x P products, gradient from M X_0)
   int32_t pad;
   uint64_t x0, x1, a, b;            // byte offsets in the workspace
   uint64_t c, m0, m1;               // Gram space: C = B A and the M ping-pong

@@ -33,8 +33,9 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 // Gram-space iteration. With M_{-1} = I every iterate is X_t = M_t X_0,
 // M_t = B_t M_{t-1}, and (all B_t being polynomials of A_0 = X_0 X_0^T, so
 // that they commute) A_{t+1} = X_t X_t^T = B_t A_t B_t: the steps need only
-// P x P products (C = B A, A = B C, M = B M; all symmetric) and X_T = M X_0
-// once at the end: per step 8 P^3 instead of 4 P^2 Q + 2 P^3 flops.
+// P x P products (C = B A, A = B C, symmetric; M = B M) and X_T = M X_0
+// once at the end (in the gradient product): per step 8 P^3 instead of
+// 4 P^2 Q + 2 P^3 flops.
 //
 // On a singular direction with normalised value x in [0, 1] (||X_0|| <= 1)
 // the matrices act as scalars: B_t = a + b y^2 + c y^4 at y = phi_{t-1}(x),
@@ -296,8 +297,8 @@ void build_plan(Plan &p) {
     }
   }
   // Update launches: the X-space updates B X (P x Q), in Gram space
-  // M = B M_prev (P x P) and X_T = M X_0 (P x Q), all full outputs, and
-  // C = B A (P x P, upper tiles, stored mirrored). The tiles of the product
+  // M = B M_prev (P x P), all full outputs, and C = B A (P x P, upper tiles,
+  // stored mirrored); the gradient product M X_0 (P x Q, full). The tiles of the product
   // that writes the trace partials of a matrix (its last X-space update; in
   // Gram space the last M = B M_prev, see Op::Update) own one slot each,
   // contiguous per matrix. A matrix's products form one job, row band by row

@@ -44,8 +44,8 @@ struct Launch {
   int32_t cfg;         // GemmCfg of a GEMM launch
   int32_t which_x;     // current X buffer (0: x0, 1: x1)
   int32_t use_a;       // update operand is A (cubic step) instead of B
-  int32_t use_m;       // update operand is M (Gram space: X_T = M X_0)
-  int32_t which_m;     // M buffer written (products) or read (X_T = M X_0)
+  int32_t use_m;       // the A operand is M (Gram-space gradient product M X_0)
+  int32_t which_m;     // M buffer written (B M products) or read (M X_0)
   int32_t which_b;     // B buffer of the step (Gram space: B_t in b[t & 1])
   int32_t m_from_b;    // M = B M_prev with M_prev = B_0 (second step: M_0 = B_0 is not stored)
   int32_t store_a0;    // first Gram: also store A_0 (Gram-space matrices)
@@ -85,7 +85,7 @@ struct Plan {
   TileRange pqm[kNumCfg];                    // later steps: also Gram-space M = B M_prev
   TileRange plast[kNumCfg];                  // Gram-space sets, last step: X-space B X and
                                              // Gram-space M = B M_prev, both with trace partials
-  TileRange fin[kNumCfg];                    // Gram space: X_T = M X_0
+  TileRange fin[kNumCfg];                    // Gram space: the gradient product M X_0
   int32_t gs_count = 0;                      // matrices iterated in Gram space
   double m_scale = 1.0;                      // scale of M in the iterate type
   TileRange prep;                      // prep tiles over Pp x Qp
