@@ -184,7 +184,7 @@ SWEEPS = {
 }
 
 
-def run_sweep(which, kind, steps, warmup, x_space=False):
+def run_sweep(which, kind, steps, warmup, gram_space=False):
     """Weight-sets/s of each set of a sweep (graph replay, inputs resident);
     one JSON line with a row per set."""
     import numpy as np
@@ -201,7 +201,7 @@ def run_sweep(which, kind, steps, warmup, x_space=False):
               else torch.from_numpy(a)).to(dev) for a in arrs]
         del arrs
         G = [torch.empty(w.shape, dtype=torch.float32, device=dev) for w in W]
-        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, x_space=x_space, device=dev)
+        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, gram_space=gram_space, device=dev)
         for _ in range(warmup):
             plan(W, G)
         torch.cuda.synchronize()
@@ -242,13 +242,15 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gram-space", action="store_true",
+                    help="skip the supplementary timing of the opt-in Gram-space schedule")
     ap.add_argument("--no-integration", action="store_true",
                     help="skip the timings of the training-loop routes (keeps profiles to the hot path)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
-    ap.add_argument("--x-space", action="store_true",
-                    help="iterate every matrix in X space (the paper's form), for comparison")
+    ap.add_argument("--gram-space", action="store_true",
+                    help="iterate the wide matrices in Gram space (opt-in, well-conditioned sets only)")
     ap.add_argument("--sweep", choices=["vit", "llm", "configs", "all"], default=None,
                     help="time every set of a sweep (App. D ViT configurations, App. F LLM shapes, "
                          "or the five configured sets) instead of the headline workload; prints one "
@@ -265,7 +267,7 @@ def main():
     from workloads import CONFIGS, make_set
 
     if args.sweep:
-        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)), args.x_space)
+        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)), args.gram_space)
         return
 
     if args.calibrate_copy:
@@ -287,7 +289,7 @@ def main():
         t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if cfg.dtype == "bf16" else torch.from_numpy(a)
         W.append(t.to(dev))
     G = [torch.empty(a.shape, dtype=torch.float32, device=dev) for a in arrs]
-    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, x_space=args.x_space, device=dev)
+    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, gram_space=args.gram_space, device=dev)
     info = plan.info()
     print(f"[bench] {cfg.name}: {cfg.n} matrices, inputs ready in {time.perf_counter() - t_gen:.1f} s, "
           f"{info['launches']} launches per step", file=sys.stderr, flush=True)
@@ -358,6 +360,30 @@ def main():
             hbm[op] = {"alg_bytes": b, "avg_ms": op_ms[op]["avg_ms"],
                        "GB/s": round(b / (op_ms[op]["avg_ms"] * 1e-3) / 1e9, 1)}
 
+    # the opt-in Gram-space schedule on the same inputs (well-conditioned sets
+    # only): its throughput, and how far its values are from the default's
+    gram_opt = None
+    if not args.gram_space and not args.no_gram_space:
+        gplan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, gram_space=True, device=dev)
+        if gplan.info()["gram_space"] > 0:
+            G2 = [torch.empty_like(g) for g in G]
+            for _ in range(args.warmup):
+                gv = gplan(W, G2)
+            torch.cuda.synchronize()
+            start.record(stream)
+            for _ in range(args.steps):
+                gv = gplan(W, G2)
+            end.record(stream)
+            torch.cuda.synchronize()
+            gms = start.elapsed_time(end) / args.steps
+            gv = gv.cpu().numpy().astype(np.float64)
+            dv = np.abs(gv[:-1] - gpu_vals[:-1]) / np.maximum(np.abs(gpu_vals[:-1]), 1e-30)
+            gram_opt = {"value": round(1000.0 / gms, 3), "ms_per_step": round(gms, 5),
+                        "gram_space_matrices": gplan.info()["gram_space"],
+                        "max_rel_value_diff_vs_default": float(dv.max()) if dv.size else 0.0}
+            del G2
+        del gplan
+
     value = 1000.0 / ms
     chain_ms = sum(op_ms[o]["ms_per_step"] for o in op_ms if o in GEMM_OPS)
     chain_alg = sum(op_ms[o]["alg_flops_per_step"] for o in op_ms if o in GEMM_OPS)
@@ -377,6 +403,7 @@ def main():
         "gemm_alg_tflops_by_op": gemm_tflops,
         "gemm_kernels": gemm_kernels,
         "gram_space_matrices": info["gram_space"],
+        "gram_space_opt_in": gram_opt,
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,
         "integration": None if args.no_integration else integration_timings(cfg, args.kind, W, G, 10),

@@ -89,9 +89,13 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
                                    iterate state and the gradient factors in the workspace; the
                                    gradient is written later by slorr_reg_grad (autograd
                                    backward, Listing 1). out_grads may be NULL. */
-#define SLORR_X_SPACE     0x20u /* iterate every matrix in X space (X <- a X + (b A + c A^2) X,
-                                   the paper's form, Sec. 3) instead of Gram space for the
-                                   wide ones (more work, the paper's rounding order) */
+#define SLORR_GRAM_SPACE  0x20u /* iterate the wide matrices (padded Q >= 2 P) in Gram space
+                                   (P x P products, fewer flops) instead of X space (the
+                                   paper's form, X <- a X + (b A + c A^2) X, Sec. 3). Opt-in:
+                                   the Gram-space state A = X X^T squares the spread of the
+                                   spectrum, so its fp16 rounding noise is amplified when
+                                   sigma_min / sigma_max falls below ~0.05 (silent errors,
+                                   NaN below ~1e-3); for well-conditioned weight sets only. */
 
 typedef struct {
   int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */

@@ -27,7 +27,7 @@ VALUES_ONLY = 0x2
 NO_GRAPH = 0x4
 AUX = 0x8
 DEFER_GRAD = 0x10
-X_SPACE = 0x20
+GRAM_SPACE = 0x20
 
 OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce",
        "grad_prod")

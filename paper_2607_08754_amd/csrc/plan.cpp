@@ -86,7 +86,7 @@ void build_plan(Plan &p) {
   if (!(p.ell > 0.0 && p.ell < 1.0)) throw std::invalid_argument("ell must be in (0, 1)");
   if (!(p.eps >= 0.0f) || !std::isfinite(p.eps)) throw std::invalid_argument("eps must be finite and >= 0");
   if (p.flags & ~uint32_t(SLORR_ACCUMULATE | SLORR_VALUES_ONLY | SLORR_NO_GRAPH | SLORR_AUX |
-                          SLORR_DEFER_GRAD | SLORR_X_SPACE))
+                          SLORR_DEFER_GRAD | SLORR_GRAM_SPACE))
     throw std::invalid_argument("unknown flag bits");
   if ((p.flags & SLORR_VALUES_ONLY) && (p.flags & SLORR_DEFER_GRAD))
     throw std::invalid_argument("SLORR_VALUES_ONLY and SLORR_DEFER_GRAD exclude each other");
@@ -109,7 +109,7 @@ void build_plan(Plan &p) {
   }
   // Gram-space iteration, for matrices with Qp >= 2 Pp (see gram_space_scale)
   double sm = 1.0;
-  const bool gs_ok = !(p.flags & SLORR_X_SPACE) && all_quintic && p.iters >= 2 &&
+  const bool gs_ok = (p.flags & SLORR_GRAM_SPACE) && all_quintic && p.iters >= 2 &&
                      gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
   p.m_scale = sm;
 

@@ -13,7 +13,7 @@ from typing import Optional, Sequence, Tuple
 import numpy as np
 
 from . import _lib
-from ._lib import ACCUMULATE, AUX, DEFER_GRAD, NO_GRAPH, VALUES_ONLY, X_SPACE, SlorrError, check, lib
+from ._lib import ACCUMULATE, AUX, DEFER_GRAD, GRAM_SPACE, NO_GRAPH, VALUES_ONLY, SlorrError, check, lib
 
 __all__ = ["Plan", "pe_coefficients", "SlorrError", "HOYER", "NUCLEAR"]
 
@@ -45,22 +45,23 @@ class Plan:
     With defer_grad=True the call writes no gradient; plan.grad(weights,
     grads, scales) writes it afterwards from the state the call left.
     grad_dtype is the element type of the gradient buffers ("f32" / "bf16").
-    x_space=True iterates every matrix in X space (the paper's form) instead
-    of Gram space for the wide ones.
+    gram_space=True iterates the wide matrices (padded Q >= 2 P) in Gram
+    space: fewer flops, for well-conditioned weights only (its fp16 state
+    loses accuracy once sigma_min / sigma_max falls below ~0.05).
     """
 
     def __init__(self, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", kind: str = HOYER,
                  iters: int = 6, degree: int = 5, ell: float = 1e-3, coeffs=None, eps: float = 0.0,
                  accumulate: bool = False, values_only: bool = False, graph: bool = True,
                  aux: bool = False, defer_grad: bool = False, grad_dtype: str = "f32",
-                 x_space: bool = False, device=None, create_workspace: bool = True):
+                 gram_space: bool = False, device=None, create_workspace: bool = True):
         self.shapes = [(int(r), int(c)) for r, c in shapes]
         self.n = len(self.shapes)
         self.dtype, self.kind, self.iters = dtype, kind, int(iters)
         self.grad_dtype = grad_dtype
         self.flags = ((ACCUMULATE if accumulate else 0) | (VALUES_ONLY if values_only else 0)
                       | (0 if graph else NO_GRAPH) | (AUX if aux else 0)
-                      | (DEFER_GRAD if defer_grad else 0) | (X_SPACE if x_space else 0))
+                      | (DEFER_GRAD if defer_grad else 0) | (GRAM_SPACE if gram_space else 0))
         self.generation = 0          # forward calls enqueued so far
         self._c_shapes = _shapes_array(self.shapes)
         if grad_dtype not in _DTYPE:

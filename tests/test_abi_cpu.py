@@ -73,7 +73,7 @@ def _tri(P, t):
     return nt * (nt + 1) / 2 * float(t) * t
 
 
-def _expected_mfma(shapes, T):
+def _expected_mfma(shapes, T, gram=False):
     """MFMA work of the schedule. Symmetric products (A, B, C) run on upper-
     triangle tiles: 256 x 256 when every matrix of the launch is 256-aligned
     and the launch has one such tile per CU for X_0 X_0^T, two per CU for the
@@ -81,9 +81,10 @@ def _expected_mfma(shapes, T):
     tiles. C = B A runs in the update launch of its step (with the X-space
     B X and, after the first step, M = B M_prev), whose tiles are 256 x 256
     when all its products allow it and it has one per CU (two in the first
-    step). Matrices with padded Q >= 2 P iterate in Gram space."""
+    step). With gram=True (the opt-in flag) matrices with padded Q >= 2 P
+    iterate in Gram space."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
-    gs = [Q >= 2 * P for P, Q in mats]
+    gs = [gram and Q >= 2 * P for P, Q in mats]
 
     def cfg(ps, min_big):
         big = sum((P // 256) * (P // 256 + 1) // 2 for P in ps)
@@ -122,20 +123,22 @@ def _expected_mfma_x(shapes, T):
     return T * sum(2 * _tri(P, 128) * Q + 2 * _tri(P, 128) * P + 2.0 * P * P * Q for P, Q in mats)
 
 
+@pytest.mark.parametrize("gram", [False, True])
 @pytest.mark.parametrize("name", list(CONFIGS))
-def test_plan_facts(L, name):
+def test_plan_facts(L, name, gram):
     cfg = CONFIGS[name]
     lib = L.lib()
     opts = L.Options()
     lib.slorr_default_options(ctypes.byref(opts))
     opts.iters = cfg.iters
+    opts.flags = L.GRAM_SPACE if gram else 0
     st, h, ws, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER, opts)
     assert st == L.OK, lib.slorr_last_error()
     info = L.PlanInfo()
     assert lib.slorr_plan_get_info(h, ctypes.byref(info)) == L.OK
     assert info.n == cfg.n and info.iters == cfg.iters
     assert info.paper_flops == pytest.approx(cfg.flops(), rel=1e-12)
-    want, ngs = _expected_mfma(cfg.shapes, cfg.iters)
+    want, ngs = _expected_mfma(cfg.shapes, cfg.iters, gram)
     assert info.gram_space == ngs
     assert info.mfma_flops == pytest.approx(want, rel=1e-12)
     assert info.mfma_flops <= info.paper_flops * (1.0 if name in ("vit_b16", "vit_l16", "llm560") else 4.0)
@@ -151,13 +154,17 @@ def test_plan_facts(L, name):
 
 def test_plan_launch_work(L):
     """slorr_plan_get_launches: one kind per launch, algorithmic flops of the
-    products each performs. Over a call: X space T (2 P^2 Q + 2 P^3 + 2 P^2 Q)
-    (the paper's count); Gram space 2 P^2 Q (X_0 X_0^T) + T 2 P^3 (poly)
-    + 3 (T - 1) 2 P^3 (C = B A, A = B C, M = B M) + 2 P^2 Q (X_T = M X_0)."""
+    products each performs. Over a call: X space (the default) T (2 P^2 Q
+    + 2 P^3 + 2 P^2 Q) (the paper's count); Gram space (opt-in, padded Q >= 2 P)
+    2 P^2 Q (X_0 X_0^T) + T 2 P^3 (poly) + 3 (T - 1) 2 P^3 (C = B A, A = B C,
+    M = B M) + 2 P^2 Q (X_T = M X_0)."""
     lib = L.lib()
-    for name in ("tiny", "resnet18", "vit_b16", "llm560"):
+    opts = L.Options()
+    for name, gram in [(n, g) for n in ("tiny", "resnet18", "vit_b16", "llm560") for g in (False, True)]:
         cfg = CONFIGS[name]
-        st, h, _, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER)
+        lib.slorr_default_options(ctypes.byref(opts))
+        opts.flags = L.GRAM_SPACE if gram else 0
+        st, h, _, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER, opts)
         assert st == L.OK
         info = L.PlanInfo()
         lib.slorr_plan_get_info(h, ctypes.byref(info))
@@ -169,14 +176,14 @@ def test_plan_launch_work(L):
         names = [L.OPS[o] for o in ops]
         gemm = ("gram", "poly", "update", "last", "grad_prod")
         assert all((e in (128, 256)) if o in gemm else e == 0 for o, e in zip(names, te))
-        ngs = sum(_pad(max(s)) >= 2 * _pad(min(s)) for s in cfg.shapes)
+        ngs = sum(gram and _pad(max(s)) >= 2 * _pad(min(s)) for s in cfg.shapes)
         tail = ["finalize", "setsum"] + ["grad_prod"] * (ngs > 0) + ["grad"] * (ngs < cfg.n)
         assert names[:3] == ["sumsq", "norm", "prep"] and names[-len(tail):] == tail
         T = info.iters                                     # the default options: T = 6
         want = 0.0
         for m, n in cfg.shapes:
             P, Q = float(min(m, n)), float(max(m, n))
-            if _pad(int(Q)) >= 2 * _pad(int(P)):
+            if gram and _pad(int(Q)) >= 2 * _pad(int(P)):
                 want += 4 * P * P * Q + 2 * P ** 3 * (T + 3 * (T - 1))
             else:
                 want += T * (4 * P * P * Q + 2 * P ** 3)
@@ -188,11 +195,14 @@ def test_plan_launch_work(L):
 
 
 def test_plan_gram_space_selection(L):
-    """Gram space is taken for padded Q >= 2 P and quintic tables only; a cubic
-    table, or a table whose M would not fit the fp16 iterate, keeps every
-    matrix in X space."""
+    """Gram space is opt-in (GRAM_SPACE) and then taken for padded Q >= 2 P and
+    quintic tables only; without the flag, with a cubic table, or with a table
+    whose M would not fit the fp16 iterate, every matrix stays in X space."""
     shapes = [(128, 256), (256, 128), (128, 255), (384, 640), (256, 256), (64, 576)]
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
+    opts = L.Options()
+    L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.flags = L.GRAM_SPACE
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
     assert st == L.OK
     info = L.PlanInfo()
     L.lib().slorr_plan_get_info(h, ctypes.byref(info))
@@ -200,9 +210,12 @@ def test_plan_gram_space_selection(L):
     # fp16 iterate: M's scale is a power of two with |M| s_m <= 2^14
     assert info.m_scale > 0 and math.log2(info.m_scale) == int(math.log2(info.m_scale))
     L.lib().slorr_plan_destroy(h)
-    opts = L.Options()
-    L.lib().slorr_default_options(ctypes.byref(opts))
-    opts.flags = L.X_SPACE                                 # the paper's form, asked for
+    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)         # the default: the paper's form
+    assert st == L.OK
+    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
+    assert info.gram_space == 0
+    L.lib().slorr_plan_destroy(h)
+    opts.flags = 0                                         # options without the flag
     st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
     assert st == L.OK
     L.lib().slorr_plan_get_info(h, ctypes.byref(info))
@@ -210,6 +223,7 @@ def test_plan_gram_space_selection(L):
     assert info.mfma_flops == pytest.approx(_expected_mfma_x(shapes, info.iters), rel=1e-12)
     L.lib().slorr_plan_destroy(h)
     L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.flags = L.GRAM_SPACE
     opts.degree = 3
     st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
     assert st == L.OK
@@ -219,6 +233,7 @@ def test_plan_gram_space_selection(L):
     # a table whose products grow beyond the fp16 range: a = 2^10 each step
     tab = (ctypes.c_double * 9)(*([1024.0, 0.0, 1e-9] * 3))
     L.lib().slorr_default_options(ctypes.byref(opts))
+    opts.flags = L.GRAM_SPACE
     opts.iters = 3
     opts.coeffs = ctypes.cast(tab, ctypes.POINTER(ctypes.c_double))
     st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
@@ -424,7 +439,10 @@ def test_split_k_gram_plan(L):
     ones; the parts cover every k exactly once (same executed MFMA work as one
     pass per tile). Sets with enough tiles are not split."""
     def facts(shapes):
-        st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
+        opts = L.Options()
+        L.lib().slorr_default_options(ctypes.byref(opts))
+        opts.flags = L.GRAM_SPACE
+        st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
         assert st == L.OK
         info = L.PlanInfo()
         L.lib().slorr_plan_get_info(h, ctypes.byref(info))
@@ -435,7 +453,7 @@ def test_split_k_gram_plan(L):
     info = facts(xs)
     assert info.gram_space == 0
     assert info.launches == 3 + 4 * T + 3                    # gram parts, reduce, poly, update
-    assert info.mfma_flops == pytest.approx(_expected_mfma(xs, T)[0], rel=1e-12)
+    assert info.mfma_flops == pytest.approx(_expected_mfma(xs, T, True)[0], rel=1e-12)
     gs = [(256, 4096), (4096, 256), (384, 2944)]             # Gram space, 3 + 3 + 6 Gram tiles
     info = facts(gs)
     assert info.gram_space == 3
@@ -444,7 +462,7 @@ def test_split_k_gram_plan(L):
     # finalize, set sum, then the gradient as the product X_T = M X_0 (no
     # gradient kernel: no X-space matrix)
     assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 3
-    assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T)[0], rel=1e-12)
+    assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T, True)[0], rel=1e-12)
     # no split: per step A, poly, one update launch (B X, B M, B A; the last
     # step's with the trace partials of both kinds); finalize, set sum, the
     # Gram-space gradient product, the X-space gradient

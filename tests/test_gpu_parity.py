@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 from parity_util import TOL, compare, run_gpu, run_oracle, to_device
-from workloads import CONFIGS, gaussian, make_set
+from workloads import CONFIGS, gaussian, make_set, with_spectrum
 
 pytestmark = pytest.mark.gpu
 
@@ -89,30 +89,51 @@ def test_ragged_shapes(dtype, kind):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("iters", [2, 3, 7])
 def test_gram_space_schedules(dtype, iters):
-    """Matrices with padded Q >= 2 P iterate in Gram space (P x P products,
-    X_T = M X_0); short and long schedules (first / middle / last step logic,
-    the M ping-pong parity), both orientations, padding, beside an X-space
-    matrix, both kinds."""
+    """gram_space=True: matrices with padded Q >= 2 P iterate in Gram space
+    (P x P products, X_T = M X_0); short and long schedules (first / middle /
+    last step logic, the M ping-pong parity), both orientations, padding,
+    beside an X-space matrix, both kinds."""
     shapes = [(96, 300), (300, 96), (128, 512), (250, 260)]
     arrs = [gaussian(s, seed=23, std=0.05, dtype=dtype, index=i) for i, s in enumerate(shapes)]
     for kind in ("hoyer", "nuclear"):
-        vals, grads, plan = run_gpu(arrs, dtype, kind, iters, eps=1e-4, g=0.8)
+        vals, grads, plan = run_gpu(arrs, dtype, kind, iters, eps=1e-4, g=0.8, gram_space=True)
         assert plan.info()["gram_space"] == 3
         refs = run_oracle(arrs, dtype, kind, iters, eps=1e-4, g=0.8)
         compare(vals, grads, refs, kind, dtype, g=0.8, label=f"gram space T={iters} {dtype} {kind}")
 
 
+@pytest.mark.parametrize("name", ["tiny", "resnet18", "vit_b16"])
+def test_gram_space_configured_sets(name):
+    """gram_space=True on configured sets that hold wide matrices (the ViT-B/16
+    set at full size, graph replay as timed), against the oracle."""
+    cfg = CONFIGS[name]
+    arrs = make_set(name, 0)
+    vals, grads, plan = run_gpu(arrs, cfg.dtype, "hoyer", cfg.iters, gram_space=True)
+    assert plan.info()["gram_space"] > 0
+    refs = run_oracle(arrs, cfg.dtype, "hoyer", cfg.iters)
+    compare(vals, grads, refs, "hoyer", cfg.dtype, label=f"{name} gram space")
+
+
+ILL = [(192, 640), (640, 192), (256, 1024), (200, 260)]
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_x_space_flag(dtype):
-    """x_space=True keeps the wide matrices in X space (the paper's form): the
-    matrices of the Gram-space test, both kinds, against the oracle."""
-    shapes = [(96, 300), (300, 96), (128, 512), (250, 260)]
-    arrs = [gaussian(s, seed=23, std=0.05, dtype=dtype, index=i) for i, s in enumerate(shapes)]
+@pytest.mark.parametrize("spectrum", ["logspace_1e-3", "rank_8"])
+def test_ill_conditioned_default_path(dtype, spectrum):
+    """The default path (X space for every matrix) on wide, tall and square
+    matrices whose singular values span three decades (log-spaced, 1 down to
+    1e-3) or that have exact rank 8: spectra on which a Gram-space iterate of
+    16 bits loses accuracy. Both kinds, against the oracle."""
+    arrs = []
+    for i, s in enumerate(ILL):
+        k = min(s)
+        sv = np.logspace(0, -3, k) if spectrum.startswith("log") else np.linspace(1.0, 0.5, 8)
+        arrs.append(with_spectrum(s, 0.05 * sv, seed=29, dtype=dtype, index=i))
     for kind in ("hoyer", "nuclear"):
-        vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=1e-4, g=0.8, x_space=True)
+        vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=1e-4, g=0.6)
         assert plan.info()["gram_space"] == 0
-        refs = run_oracle(arrs, dtype, kind, 6, eps=1e-4, g=0.8)
-        compare(vals, grads, refs, kind, dtype, g=0.8, label=f"x space {dtype} {kind}")
+        refs = run_oracle(arrs, dtype, kind, 6, eps=1e-4, g=0.6)
+        compare(vals, grads, refs, kind, dtype, g=0.6, label=f"{spectrum} {dtype} {kind}")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

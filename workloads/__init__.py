@@ -61,6 +61,17 @@ def gaussian(shape: Shape, seed: int, std: float, dtype: str = "f32", index: int
     return _store(_rng(seed, index).standard_normal(shape) * std, dtype)
 
 
+def with_spectrum(shape: Shape, svals, seed: int, dtype: str = "f32", index: int = 0) -> np.ndarray:
+    """U diag(svals) V^T with Haar-random orthonormal U (rows x k) and V
+    (cols x k), k = len(svals) <= min(shape): a matrix of prescribed singular
+    values (rank k when k < min(shape)), stored as `dtype`."""
+    rng = _rng(seed, index)
+    s = np.asarray(svals, dtype=np.float64)
+    U = _haar_cols(rng, shape[0], len(s))
+    V = _haar_cols(rng, shape[1], len(s))
+    return _store((U * s[None, :]) @ V.T, dtype)
+
+
 # ---------------------------------------------------------------- generators
 
 def _gen_gauss(std_of: Callable[[Shape], float]):
