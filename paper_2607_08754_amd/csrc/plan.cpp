@@ -166,7 +166,7 @@ void build_plan(Plan &p) {
     r.first = int32_t(p.tiles.size());
     if (whole.empty()) return r;
     // a set of few large matrices would leave XCDs idle: cut every matrix into
-    // jobs of at most 1/16 of the launch's tiles (whole row bands first)
+    // jobs of at most 1/16 of the launch's tiles (contiguous runs of its tile order)
     size_t total = 0;
     for (const Job &j : whole) total += j.tiles.size();
     const size_t cap = std::max<size_t>(1, (total + 2 * kXcds - 1) / (2 * kXcds));
@@ -330,13 +330,25 @@ void build_plan(Plan &p) {
       MatDesc &d = p.mats[prods[f].mat];
       Job j{prods[f].mat, double(d.Pp), {}};
       if (slots) d.trace_begin = slot;
-      for (int tm = 0; tm < d.Pp / ts; ++tm)
+      auto add = [&](size_t q, int tm, int tn) {
+        Tile t = make_tile(prods[q].mat, tm, tn, slots ? slot++ : 0);
+        t.op = prods[q].op;
+        j.tiles.push_back(t);
+      };
+      bool any_upper = false;
+      for (size_t q = f; q < e; ++q) any_upper |= prods[q].upper;
+      if (!any_upper) {
+        // column panel by column panel: the Pp / ts tiles that read one panel
+        // of the right operand are dispatched together on one XCD, so the
+        // panel is fetched into its L2 once
         for (size_t q = f; q < e; ++q)
-          for (int tn = prods[q].upper ? tm : 0; tn < prods[q].n / ts; ++tn) {
-            Tile t = make_tile(prods[q].mat, tm, tn, slots ? slot++ : 0);
-            t.op = prods[q].op;
-            j.tiles.push_back(t);
-          }
+          for (int tn = 0; tn < prods[q].n / ts; ++tn)
+            for (int tm = 0; tm < d.Pp / ts; ++tm) add(q, tm, tn);
+      } else {
+        for (int tm = 0; tm < d.Pp / ts; ++tm)
+          for (size_t q = f; q < e; ++q)
+            for (int tn = prods[q].upper ? tm : 0; tn < prods[q].n / ts; ++tn) add(q, tm, tn);
+      }
       if (slots) d.trace_end = slot;
       jobs.push_back(std::move(j));
       f = e;

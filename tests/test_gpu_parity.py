@@ -5,8 +5,8 @@ gradients), for every configured weight set and the edge cases.
 import numpy as np
 import pytest
 
-from parity_util import TOL, compare, run_gpu, run_oracle, to_device
-from workloads import CONFIGS, gaussian, make_set, with_spectrum
+from parity_util import TOL, compare, grad_err, run_gpu, run_oracle, to_device, value_err
+from workloads import CONFIGS, gaussian, make_set, widen, with_spectrum
 
 pytestmark = pytest.mark.gpu
 
@@ -118,22 +118,57 @@ ILL = [(192, 640), (640, 192), (256, 1024), (200, 260)]
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("spectrum", ["logspace_1e-3", "rank_8"])
-def test_ill_conditioned_default_path(dtype, spectrum):
+def test_ill_conditioned_default_path(dtype):
     """The default path (X space for every matrix) on wide, tall and square
     matrices whose singular values span three decades (log-spaced, 1 down to
-    1e-3) or that have exact rank 8: spectra on which a Gram-space iterate of
-    16 bits loses accuracy. Both kinds, against the oracle."""
-    arrs = []
-    for i, s in enumerate(ILL):
-        k = min(s)
-        sv = np.logspace(0, -3, k) if spectrum.startswith("log") else np.linspace(1.0, 0.5, 8)
-        arrs.append(with_spectrum(s, 0.05 * sv, seed=29, dtype=dtype, index=i))
+    1e-3): a spectrum on which a Gram-space iterate of 16 bits loses accuracy.
+    Both kinds, against the oracle."""
+    arrs = [with_spectrum(s, 0.05 * np.logspace(0, -3, min(s)), seed=29, dtype=dtype, index=i)
+            for i, s in enumerate(ILL)]
     for kind in ("hoyer", "nuclear"):
         vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=1e-4, g=0.6)
         assert plan.info()["gram_space"] == 0
         refs = run_oracle(arrs, dtype, kind, 6, eps=1e-4, g=0.6)
-        compare(vals, grads, refs, kind, dtype, g=0.6, label=f"{spectrum} {dtype} {kind}")
+        compare(vals, grads, refs, kind, dtype, g=0.6, label=f"logspace {dtype} {kind}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rank_deficient_default_path(dtype):
+    """Rank 8 (singular values 0.05 down to 0.025) on wide, tall and square
+    matrices. The approximation guarantee covers the nonzero singular subspace
+    only (App. C, the remark on zero singular values): the stored matrix has
+    rounding-sized singular values far below ell in the other directions, and
+    there the iteration scales the rounding noise of any finite-precision
+    iterate by about the product of the a_t (about 2000 for T = 6), so the
+    block of the gradient on the two null spaces is not fixed by the method.
+    Checked: the values, and the gradient with that block removed, against the
+    oracle at the usual tolerance; that block's spectral norm at most
+    1.25 s1 (the polar factor's block is a contraction up to the overshoot of
+    the polynomials)."""
+    r, g, eps = 8, 0.6, 1e-4
+    arrs = [with_spectrum(s, 0.05 * np.linspace(1.0, 0.5, r), seed=31, dtype=dtype, index=i)
+            for i, s in enumerate(ILL)]
+    tol = TOL[dtype]
+    for kind in ("hoyer", "nuclear"):
+        vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=eps, g=g)
+        assert plan.info()["gram_space"] == 0
+        refs = run_oracle(arrs, dtype, kind, 6, eps=eps, g=g)
+        for i, (a, G, ref) in enumerate(zip(arrs, grads, refs)):
+            U, _, Vt = np.linalg.svd(widen(a, dtype).astype(np.float64), full_matrices=False)
+            Nu = np.eye(a.shape[0]) - U[:, :r] @ U[:, :r].T
+            Nv = np.eye(a.shape[1]) - Vt[:r].T @ Vt[:r]
+            nn = Nu @ G @ Nv
+            ve = value_err(vals[i], ref)
+            s1 = 2.0 * g * ref.n_hat / ref.f_eps ** 2 if kind == "hoyer" else g
+            den = max(np.linalg.norm(ref.grad), np.linalg.norm(s1 * ref.polar))
+            ge = np.linalg.norm((G - nn) - (ref.grad - Nu @ ref.grad @ Nv)) / den
+            full = grad_err(G, ref, kind, g)
+            bound = np.linalg.norm(nn, 2) / s1
+            print(f"[parity] rank {r} {dtype} {kind} {a.shape}: value err {ve:.2e}, grad err off the "
+                  f"null block {ge:.2e} (full {full:.2e}), null block norm / s1 {bound:.3f}", flush=True)
+            assert np.isfinite(vals[i]) and ve <= tol, (i, ve)
+            assert ge <= tol, (i, ge)
+            assert bound <= 1.25, (i, bound)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
