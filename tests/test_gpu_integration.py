@@ -48,14 +48,19 @@ def _mat(t):
     return t.detach().reshape(t.shape[0], -1).float().cpu().numpy().astype(np.float64)
 
 
+@pytest.mark.parametrize("gram_space", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("kind", ["hoyer", "nuclear"])
-def test_autograd_matches_oracle(dtype, kind):
+def test_autograd_matches_oracle(dtype, kind, gram_space):
+    """Both schedules: with gram_space=True the two matrices with padded
+    Q >= 2 P (96 x 160, 200 x 72) take Gram space and the deferred gradient
+    replays its gradient product."""
     import torch
     from paper_2607_08754_amd import Regularizer
     arrs = _arrays(dtype, 11)
     params = _params(arrs, dtype)
-    reg = Regularizer(params, kind=kind)
+    reg = Regularizer(params, kind=kind, gram_space=gram_space)
+    assert reg.plan("autograd").info()["gram_space"] == (2 if gram_space else 0)
     c = torch.tensor([0.5, -1.25, 2.0, 1.0], device=DEV)
     L = reg.loss()
     (L * c).sum().backward()
@@ -64,7 +69,8 @@ def test_autograd_matches_oracle(dtype, kind):
     for i, a in enumerate(arrs):
         ref = fwd_bwd(widen(a, dtype), kind, TABLE, g=float(c[i]))
         ve, ge = value_err(vals[i], ref), grad_err(_mat(params[i].grad), ref, kind, g=float(c[i]))
-        print(f"[integration] autograd {dtype} {kind} matrix {i} {SHAPES[i]}: value {ve:.2e} grad {ge:.2e}",
+        print(f"[integration] autograd {dtype} {kind} gram_space={gram_space} matrix {i} {SHAPES[i]}: "
+              f"value {ve:.2e} grad {ge:.2e}",
               flush=True)
         assert params[i].grad.dtype == params[i].dtype and params[i].grad.shape == params[i].shape
         assert ve <= TOL[dtype] and ge <= TOL[dtype]
