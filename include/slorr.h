@@ -93,9 +93,10 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
                                    (P x P products, fewer flops) instead of X space (the
                                    paper's form, X <- a X + (b A + c A^2) X, Sec. 3). Opt-in:
                                    the Gram-space state A = X X^T squares the spread of the
-                                   spectrum, so its fp16 rounding noise is amplified when
-                                   sigma_min / sigma_max falls below ~0.05 (silent errors,
-                                   NaN below ~1e-3); for well-conditioned weight sets only. */
+                                   spectrum, so its fp16 rounding noise is amplified as
+                                   sigma_min / sigma_max falls: errors past the bf16
+                                   tolerance (2e-2) from a spread of ~0.1 on some shapes,
+                                   NaN near 1e-4. For well-conditioned weight sets only. */
 
 typedef struct {
   int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */

@@ -47,7 +47,8 @@ class Plan:
     grad_dtype is the element type of the gradient buffers ("f32" / "bf16").
     gram_space=True iterates the wide matrices (padded Q >= 2 P) in Gram
     space: fewer flops, for well-conditioned weights only (its fp16 state
-    loses accuracy once sigma_min / sigma_max falls below ~0.05).
+    loses accuracy as sigma_min / sigma_max falls: past 2e-2 from ~0.1 on
+    some shapes).
     """
 
     def __init__(self, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", kind: str = HOYER,

@@ -114,6 +114,21 @@ def test_gram_space_configured_sets(name):
     compare(vals, grads, refs, "hoyer", cfg.dtype, label=f"{name} gram space")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gram_space_well_conditioned_spectrum(dtype):
+    """gram_space=True inside its range of validity: wide and tall matrices
+    whose singular values are log-spaced from 1 down to sigma_min / sigma_max
+    = 0.3, both kinds, against the oracle at the usual tolerance."""
+    shapes = [(256, 1024), (1024, 256), (192, 640)]
+    arrs = [with_spectrum(s, 0.05 * np.logspace(0, np.log10(0.3), min(s)), seed=37, dtype=dtype, index=i)
+            for i, s in enumerate(shapes)]
+    for kind in ("hoyer", "nuclear"):
+        vals, grads, plan = run_gpu(arrs, dtype, kind, 6, eps=1e-4, g=0.9, gram_space=True)
+        assert plan.info()["gram_space"] == 3
+        refs = run_oracle(arrs, dtype, kind, 6, eps=1e-4, g=0.9)
+        compare(vals, grads, refs, kind, dtype, g=0.9, label=f"gram space, spread 0.3, {dtype} {kind}")
+
+
 ILL = [(192, 640), (640, 192), (256, 1024), (200, 260)]
 
 
