@@ -260,7 +260,8 @@ typedef struct {
   double weight_bytes;     /* sum_i rows_i * cols_i * sizeof(dtype)                  */
   size_t workspace_bytes;
   int32_t gram_space;      /* matrices iterated in Gram space (P x P products, the   */
-                           /* gradient from M X_0; padded Q >= 2 P, quintic tables)  */
+                           /* gradient from M X_0): 0 unless SLORR_GRAM_SPACE is set; */
+                           /* then those with padded Q >= 2 P, quintic tables only    */
   double m_scale;          /* scale of M in the iterate type                         */
 } slorr_plan_info_t;
 
