@@ -107,7 +107,8 @@ void build_plan(Plan &p) {
     any_quintic |= p.coeffs[3 * t + 2] != 0.0;
     all_quintic &= p.coeffs[3 * t + 2] != 0.0;
   }
-  // Gram-space iteration, for matrices with Qp >= 2 Pp (see gram_space_scale)
+  // Gram-space iteration (opt-in: its 16-bit state loses accuracy on
+  // ill-conditioned spectra), for matrices with Qp >= 2 Pp (see gram_space_scale)
   double sm = 1.0;
   const bool gs_ok = (p.flags & SLORR_GRAM_SPACE) && all_quintic && p.iters >= 2 &&
                      gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
