@@ -27,30 +27,35 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}     # dense MFMA: fp16/bf16 operands, fp32 operands
-GEMM_OPS = ("gram", "poly", "update", "last", "grad_prod")
-# kernel mode of each product launch kind
-KERNEL_MODE = {"gram": "gram", "poly": "poly", "update": "update", "last": "last", "grad_prod": "grad"}
+GEMM_OPS = ("gram", "poly", "update", "last")
 
 
 def kernel_instance(op, edge):
     """Name of the GEMM kernel instance a launch runs: mode and block tile."""
-    return f"k_gemm<{KERNEL_MODE[op]}, {edge}x{edge}>"
+    return f"k_gemm<{op}, {edge}x{edge}>"
 
 
-def _alg_bytes_per_launch(shapes, dtype, op, gram_space):
+def _alg_bytes_per_launch(shapes, dtype, op):
     """Bytes the memory-bound kernels must move: sumsq reads W (a2); prep reads W
-    and writes X_0 (a3); grad reads W and P and writes the fp32 gradient (a7)
-    of the matrices iterated in X space (a Gram-space matrix's gradient is
-    written by its last product)."""
+    and writes X_0 (a3); grad reads W and P and writes the fp32 gradient (a7)."""
     wb = 2 if dtype == "bf16" else 4          # weight element
     xb = 2 if dtype == "bf16" else 4          # iterate element (fp16 / fp32)
-    pad = lambda x: (x + 127) // 128 * 128
     tot = 0
     for m, n in shapes:
         e = m * n
-        gs = gram_space and pad(max(m, n)) >= 2 * pad(min(m, n))
-        tot += {"sumsq": wb * e, "prep": (wb + xb) * e, "grad": 0 if gs else (wb + xb + 4) * e}[op]
+        tot += {"sumsq": wb * e, "prep": (wb + xb) * e, "grad": (wb + xb + 4) * e}[op]
     return float(tot)
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def integration_timings(cfg, kind, W, G, steps):
@@ -138,24 +143,24 @@ def _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
     returns (blocks done, blocks in the set, seconds, worst value / gradient
     error of the GPU output on the sampled matrices)."""
     import numpy as np
-    from oracle.pe_schedule import pe_schedule
+    from oracle.pe_schedule import default_table
     from oracle.slorr import fwd_bwd
     from workloads import widen
-    table = pe_schedule(cfg.iters)
+    table = default_table(cfg.iters)
     per_block = cfg.block
     nblocks = cfg.n // per_block
-    done, worst_v, worst_g = 0, 0.0, 0.0
+    done, worst_v, worst_g, worst_m = 0, 0.0, 0.0, 0.0
     t0 = time.perf_counter()
     while done < nblocks and (time.perf_counter() - t0) < seconds:
         for i in range(done * per_block, (done + 1) * per_block):
             W = widen(arrs[i], cfg.dtype)
             r = fwd_bwd(W, kind, table)
             worst_v = max(worst_v, abs(gpu_vals[i] - r.value) / abs(r.value))
-            s1 = 2.0 * r.n_hat / r.f_eps ** 2 if kind == "hoyer" else 1.0
-            den = max(np.linalg.norm(r.grad), np.linalg.norm(s1 * r.polar))
-            worst_g = max(worst_g, float(np.linalg.norm(gpu_grads[i] - r.grad) / den))
+            d = gpu_grads[i] - r.grad
+            worst_g = max(worst_g, float(np.linalg.norm(d) / np.linalg.norm(r.grad)))
+            worst_m = max(worst_m, float(np.abs(d).max() / np.abs(r.grad).max()))
         done += 1
-    return done, nblocks, per_block, time.perf_counter() - t0, worst_v, worst_g
+    return done, nblocks, per_block, time.perf_counter() - t0, worst_v, (worst_g, worst_m)
 
 
 def cpu_baseline(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
@@ -168,12 +173,13 @@ def cpu_baseline(cfg, arrs, kind, gpu_vals, gpu_grads, seconds):
     with threadpool_limits(limits=1, user_api="blas"):
         d1, _, _, el1, _, _ = _run_oracle(cfg, arrs, kind, gpu_vals, gpu_grads, seconds / 2)
     return {"value": done * per_block / cfg.n / el, "unit": "weight-sets/s", "cores": int(cores),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": _cpu_model(),
             "sample": f"{done} of {nblocks} blocks ({done * per_block} of {cfg.n} matrices), "
                       f"NumPy float64, {el:.1f} s",
             "one_core": {"value": d1 * per_block / cfg.n / el1, "unit": "weight-sets/s",
                          "sample": f"{d1} of {nblocks} blocks, {el1:.1f} s"},
-            "parity_on_sample": {"max_value_rel_err": wv, "max_grad_rel_err": wg}}
+            "parity_on_sample": {"max_value_rel_err": wv, "max_grad_rel_err": wg[0],
+                                 "max_grad_elementwise_rel_err": wg[1]}}
 
 
 SWEEPS = {
@@ -184,7 +190,7 @@ SWEEPS = {
 }
 
 
-def run_sweep(which, kind, steps, warmup, gram_space=False):
+def run_sweep(which, kind, steps, warmup):
     """Weight-sets/s of each set of a sweep (graph replay, inputs resident);
     one JSON line with a row per set."""
     import numpy as np
@@ -201,7 +207,7 @@ def run_sweep(which, kind, steps, warmup, gram_space=False):
               else torch.from_numpy(a)).to(dev) for a in arrs]
         del arrs
         G = [torch.empty(w.shape, dtype=torch.float32, device=dev) for w in W]
-        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, gram_space=gram_space, device=dev)
+        plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=kind, iters=cfg.iters, device=dev)
         for _ in range(warmup):
             plan(W, G)
         torch.cuda.synchronize()
@@ -221,7 +227,6 @@ def run_sweep(which, kind, steps, warmup, gram_space=False):
                       "paper_frac_of_peak": round(tf / peak, 4),
                       "alg_tflop_per_set": round(alg / 1e12, 4),
                       "alg_tflops": round(alg / (ms * 1e-3) / 1e12, 1),
-                      "gram_space_matrices": plan.info()["gram_space"],
                       "mfma_flops_per_set": plan.info()["mfma_flops"]}
         print(f"[sweep] {name}: {ms:.3f} ms/set, {tf:.0f} TFLOP/s (paper count)", file=sys.stderr, flush=True)
         plan.close()
@@ -242,15 +247,11 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-gram-space", action="store_true",
-                    help="skip the supplementary timing of the opt-in Gram-space schedule")
     ap.add_argument("--no-integration", action="store_true",
                     help="skip the timings of the training-loop routes (keeps profiles to the hot path)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (reference for the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
-    ap.add_argument("--gram-space", action="store_true",
-                    help="iterate the wide matrices in Gram space (opt-in, well-conditioned sets only)")
     ap.add_argument("--sweep", choices=["vit", "llm", "configs", "all"], default=None,
                     help="time every set of a sweep (App. D ViT configurations, App. F LLM shapes, "
                          "or the five configured sets) instead of the headline workload; prints one "
@@ -267,7 +268,7 @@ def main():
     from workloads import CONFIGS, make_set
 
     if args.sweep:
-        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)), args.gram_space)
+        run_sweep(args.sweep, args.kind, max(1, min(args.steps, 20)), max(1, min(args.warmup, 3)))
         return
 
     if args.calibrate_copy:
@@ -289,7 +290,7 @@ def main():
         t = torch.from_numpy(a.view(np.int16)).view(torch.bfloat16) if cfg.dtype == "bf16" else torch.from_numpy(a)
         W.append(t.to(dev))
     G = [torch.empty(a.shape, dtype=torch.float32, device=dev) for a in arrs]
-    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, gram_space=args.gram_space, device=dev)
+    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, device=dev)
     info = plan.info()
     print(f"[bench] {cfg.name}: {cfg.n} matrices, inputs ready in {time.perf_counter() - t_gen:.1f} s, "
           f"{info['launches']} launches per step", file=sys.stderr, flush=True)
@@ -298,13 +299,16 @@ def main():
     for _ in range(args.warmup):
         vals = plan(W, G)
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for _ in range(args.steps):
+    # K replays between two synchronisations; an event between consecutive
+    # replays gives each one's duration (median, p10, p90)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record(stream)
+    for k in range(args.steps):
         vals = plan(W, G)
-    end.record(stream)
+        evs[k + 1].record(stream)
     torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    step_ms = np.array([evs[k].elapsed_time(evs[k + 1]) for k in range(args.steps)])
     gpu_vals = vals.cpu().numpy().astype(np.float64)
     print(f"[bench] timed {args.steps} steps: {ms:.4f} ms/step", file=sys.stderr, flush=True)
 
@@ -356,33 +360,9 @@ def main():
     hbm = {}
     for op in ("sumsq", "prep", "grad"):
         if op in op_ms:
-            b = _alg_bytes_per_launch(cfg.shapes, cfg.dtype, op, info["gram_space"] > 0)
+            b = _alg_bytes_per_launch(cfg.shapes, cfg.dtype, op)
             hbm[op] = {"alg_bytes": b, "avg_ms": op_ms[op]["avg_ms"],
                        "GB/s": round(b / (op_ms[op]["avg_ms"] * 1e-3) / 1e9, 1)}
-
-    # the opt-in Gram-space schedule on the same inputs (well-conditioned sets
-    # only): its throughput, and how far its values are from the default's
-    gram_opt = None
-    if not args.gram_space and not args.no_gram_space:
-        gplan = Plan(cfg.shapes, dtype=cfg.dtype, kind=args.kind, iters=cfg.iters, gram_space=True, device=dev)
-        if gplan.info()["gram_space"] > 0:
-            G2 = [torch.empty_like(g) for g in G]
-            for _ in range(args.warmup):
-                gv = gplan(W, G2)
-            torch.cuda.synchronize()
-            start.record(stream)
-            for _ in range(args.steps):
-                gv = gplan(W, G2)
-            end.record(stream)
-            torch.cuda.synchronize()
-            gms = start.elapsed_time(end) / args.steps
-            gv = gv.cpu().numpy().astype(np.float64)
-            dv = np.abs(gv[:-1] - gpu_vals[:-1]) / np.maximum(np.abs(gpu_vals[:-1]), 1e-30)
-            gram_opt = {"value": round(1000.0 / gms, 3), "ms_per_step": round(gms, 5),
-                        "gram_space_matrices": gplan.info()["gram_space"],
-                        "max_rel_value_diff_vs_default": float(dv.max()) if dv.size else 0.0}
-            del G2
-        del gplan
 
     value = 1000.0 / ms
     chain_ms = sum(op_ms[o]["ms_per_step"] for o in op_ms if o in GEMM_OPS)
@@ -396,14 +376,15 @@ def main():
                                f"{cfg.dtype} weights, T={cfg.iters}, {args.kind}",
                    "matrices": cfg.n, "iters": cfg.iters, "kind": args.kind},
         "roofline": roofline,
+        "step_ms": {"median": round(float(np.median(step_ms)), 5), "p10": round(float(np.percentile(step_ms, 10)), 5),
+                    "p90": round(float(np.percentile(step_ms, 90)), 5),
+                    "sets_per_s_at_median": round(1000.0 / float(np.median(step_ms)), 3)},
         "matrices_per_s": round(cfg.n * value, 1),
         "paper_tflops_effective": round(cfg.flops() / (ms * 1e-3) / 1e12, 2),
         "gemm_chain_frac_of_peak": round(cfg.flops() / (chain_ms * 1e-3) / 1e12 / peak, 4),
         "gemm_chain_alg_tflops": round(chain_alg / (chain_ms * 1e-3) / 1e12, 1),
         "gemm_alg_tflops_by_op": gemm_tflops,
         "gemm_kernels": gemm_kernels,
-        "gram_space_matrices": info["gram_space"],
-        "gram_space_opt_in": gram_opt,
         "per_op_ms": {k: round(v["ms_per_step"], 4) for k, v in op_ms.items()},
         "hbm_kernels": hbm,
         "integration": None if args.no_integration else integration_timings(cfg, args.kind, W, G, 10),

@@ -29,7 +29,8 @@
  *
  * Execution model
  *   - The caller owns every device buffer (weights, gradients, values and the
- *     workspace). The library allocates no device memory.
+ *     workspace). The library allocates device memory only for the plans of
+ *     its internal cache (slorr_reg_fwd_bwd with plan == NULL).
  *   - Work is enqueued asynchronously on the caller's HIP stream. Validation is
  *     complete before anything is enqueued: a non-OK status means nothing was
  *     enqueued. Device faults surface on a later HIP call as SLORR_ERR_HIP.
@@ -89,14 +90,6 @@ typedef struct { int32_t rows, cols; } slorr_shape_t;
                                    iterate state and the gradient factors in the workspace; the
                                    gradient is written later by slorr_reg_grad (autograd
                                    backward, Listing 1). out_grads may be NULL. */
-#define SLORR_GRAM_SPACE  0x20u /* iterate the wide matrices (padded Q >= 2 P) in Gram space
-                                   (P x P products, fewer flops) instead of X space (the
-                                   paper's form, X <- a X + (b A + c A^2) X, Sec. 3). Opt-in:
-                                   the Gram-space state A = X X^T squares the spread of the
-                                   spectrum, so its fp16 rounding noise is amplified as
-                                   sigma_min / sigma_max falls: errors past the bf16
-                                   tolerance (2e-2) from a spread of ~0.1 on some shapes,
-                                   NaN near 1e-4. For well-conditioned weight sets only. */
 
 typedef struct {
   int32_t iters;         /* T >= 1 Polar Express steps; 0 -> 6 (App. E.1)                    */
@@ -109,12 +102,18 @@ typedef struct {
   uint32_t flags;        /* SLORR_* flags above                                              */
   slorr_dtype_t grad_dtype; /* element type of the gradient buffers: F32 (default) or BF16
                             (round to nearest even; for bf16 models whose .grad is bf16) */
+  double safety;         /* stabilisation of the built-in schedule (the paper's unspecified
+                            Polar Express stabilisations, read as its safety factor): every
+                            step but the last evaluates p_t(x / (1 + safety)), so that the
+                            rounding of the 16-bit or fp32 iterate cannot push a singular
+                            value past the next step's interval; 0 -> 0.01, < 0 -> none,
+                            else in (0, 1). Not applied to an explicit coeffs table.   */
 } slorr_options_t;
 
 typedef struct slorr_plan_s *slorr_plan_t;
 
 /* Fill *opts with the defaults: iters 6, degree 5, ell 1e-3, coeffs NULL,
- * eps 0, flags 0, grad_dtype F32. */
+ * eps 0, flags 0, grad_dtype F32, safety 0.01. */
 SLORR_API void slorr_default_options(slorr_options_t *opts);
 
 /* Greedy Polar Express schedule (Sec. 3; App. E.1), host only, no device use.
@@ -124,26 +123,44 @@ SLORR_API void slorr_default_options(slorr_options_t *opts);
  * minimax problem is below double-precision resolution) every later step uses
  * the limit polynomial of the recursion, Newton-Schulz: (15x - 10x^3 + 3x^5)/8
  * for degree 5, (3x - x^3)/2 for degree 3. Writes iters rows (a_t, b_t, c_t)
- * to out (host array of 3*iters doubles; c_t = 0 for degree 3). */
+ * to out (host array of 3*iters doubles; c_t = 0 for degree 3): the greedy
+ * rows themselves, before the stabilisation a plan applies (options.safety). */
 SLORR_API slorr_status_t slorr_pe_coefficients(double ell, int32_t degree, int32_t iters, double *out);
 
-/* Build a plan for a fixed set of n matrices (host only, no device use).
- * shapes: host array of n shapes. n >= 0 (n == 0 is a valid empty set).
- * opts may be NULL (defaults). *workspace_bytes receives the size of the
- * device workspace the plan needs (never 0). On error *plan is set to NULL. */
-SLORR_API slorr_status_t slorr_plan_create(slorr_plan_t *plan, int32_t n, const slorr_shape_t *shapes,
-                                 slorr_dtype_t dtype, slorr_kind_t kind,
-                                 const slorr_options_t *opts, size_t *workspace_bytes);
+/* Build a plan for a fixed set of n matrices (host only, no device use): the
+ * canonical orientation of every matrix (Sec. 3 "Computational cost": the
+ * products are formed on the short side), the shape grouping, the launch
+ * schedule of the T Polar Express steps (Sec. 3; App. E.1) and the workspace
+ * layout.
+ *   plan            : out; receives the handle (NULL on error)
+ *   n, shapes       : host array of n shapes; n >= 0 (n == 0 is a valid empty set)
+ *   dtype, kind     : weight storage type; regularizer
+ *   opts            : may be NULL (defaults, see slorr_default_options)
+ *   workspace_bytes : out; size of the device workspace the plan needs (never 0)
+ * Errors: INVALID_ARGUMENT (NULL pointers, negative sizes, bad options),
+ * UNSUPPORTED (dtype / kind / degree, sizes beyond the limits). */
+SLORR_API slorr_status_t slorr_plan(slorr_plan_t *plan, int32_t n, const slorr_shape_t *shapes,
+                                    slorr_dtype_t dtype, slorr_kind_t kind,
+                                    const slorr_options_t *opts, size_t *workspace_bytes);
 
 /* Attach caller-owned device memory as the plan's workspace. dev_ptr must be
- * 256-byte aligned and at least the size slorr_plan_create reported. The
+ * 256-byte aligned and at least the size slorr_plan reported. The
  * library writes its static tables into it (synchronous host-to-device copy on
  * the current device) and keeps the pointer until the next call to this
  * function or slorr_plan_destroy; the caller keeps the memory alive that long.
  * The current device at this call is the plan's device. */
 SLORR_API slorr_status_t slorr_plan_set_workspace(slorr_plan_t plan, void *dev_ptr, size_t bytes);
 
-/* Forward + backward of the regularizer over the whole set.
+/* Forward + backward of the regularizer over the whole set (Sec. 3: the value
+ * of Listing 1's forward and the gradient of Eq. SLORR_grads; App. E.3 with
+ * SLORR_ACCUMULATE).
+ *   plan      : a plan with a workspace, or NULL: then the library's internal
+ *               plan cache supplies one for (current device, stream, the
+ *               calling thread's slorr_cache_config dtype and options, kind,
+ *               iters, shapes), creating it with a workspace it allocates itself
+ *               (hipMalloc) on first use; the cache keeps up to 8 plans, least
+ *               recently used evicted (that eviction synchronises the device and
+ *               frees the workspace). Calls on the cache are serialised by a lock.
  *   n, shapes, kind, iters : must equal the plan's (SLORR_ERR_PLAN_MISMATCH)
  *   weights   : host array of n device pointers, weights[i] -> rows_i x cols_i
  *               row-major contiguous values of the plan's dtype, 16-byte aligned
@@ -173,9 +190,19 @@ SLORR_API slorr_status_t slorr_reg_fwd_bwd(slorr_plan_t plan, int32_t n, const v
                                  float *out_vals, void *const *out_grads, float grad_scale,
                                  void *stream);
 
+/* dtype and options (the opts fields other than iters, which the call gives)
+ * used by slorr_reg_fwd_bwd calls with plan == NULL from the calling thread.
+ * Until the first call the defaults are F32 and slorr_default_options. opts
+ * may be NULL (defaults); a coefficient table is copied. Host only. */
+SLORR_API void slorr_cache_config(slorr_dtype_t dtype, const slorr_options_t *opts);
+
+/* Release every plan of the internal cache and its workspace (synchronises
+ * the devices they run on). Host only; the cache refills on the next NULL-plan
+ * call. */
+SLORR_API slorr_status_t slorr_cache_clear(void);
+
 /* Gradient from the state a preceding slorr_reg_fwd_bwd on this plan left in
- * the workspace (the last iterate P of X-space matrices, M_{T-1} and X_0 of
- * Gram-space ones, and the factors s1, s2): the backward half of a forward
+ * the workspace (the last iterate P and the factors s1, s2): the backward half of a forward
  * run with SLORR_DEFER_GRAD (or any run that wrote gradients). It runs the
  * same gradient launches as the one-call path.
  *   n, weights, shapes, kind, iters : as in that call; weights must hold the
@@ -216,19 +243,18 @@ SLORR_API slorr_status_t slorr_decoupled_apply(slorr_plan_t plan, int32_t n, voi
 /* Kernel kinds of the launch schedule, as reported by slorr_reg_fwd_bwd_profiled. */
 typedef enum {
   SLORR_OP_SUMSQ = 0,     /* partial sums of W^2 per chunk               */
-  SLORR_OP_NORM = 1,      /* ||W||_F and ||W||_F + eps per matrix         */
-  SLORR_OP_PREP = 2,      /* X_0 = W / (||W||_F + eps), short-side layout */
-  SLORR_OP_GRAM = 3,      /* A = X X^T; Gram space: A = B C               */
-  SLORR_OP_POLY = 4,      /* B = b_t A + c_t A A                          */
-  SLORR_OP_UPDATE = 5,    /* X = a_t X + B X; Gram space: M = B M_prev,   */
-                          /* C = B A                                      */
-  SLORR_OP_LAST = 6,      /* last update: P and the trace partials (Gram  */
-                          /* space: the last M, trace tr(M A_0))          */
+  SLORR_OP_NORM = 1,      /* ||W||_F, ||W||_F + eps and the split of its  */
+                          /* inverse into 2^-e and kappa, per matrix      */
+  SLORR_OP_PREP = 2,      /* X_0' = W / 2^e, short-side layout (the first */
+                          /* step applies kappa = 2^e / (||W||_F + eps))  */
+  SLORR_OP_GRAM = 3,      /* A = X X^T                                    */
+  SLORR_OP_POLY = 4,      /* B = a_t I + b_t A + c_t A A                  */
+  SLORR_OP_UPDATE = 5,    /* X = B X  (cubic steps: a_t X + b_t A X)      */
+  SLORR_OP_LAST = 6,      /* last update: P and the trace partials        */
   SLORR_OP_FINALIZE = 7,  /* values and gradient factors per matrix       */
   SLORR_OP_GRAD = 8,      /* gradient epilogue                            */
   SLORR_OP_SETSUM = 9,    /* the set total, summed in index order         */
-  SLORR_OP_GRAM_REDUCE = 10, /* sum of split-K Gram partials, A = X X^T    */
-  SLORR_OP_GRAD_PROD = 11 /* Gram space: gradient g (s1 M X_0 - s2 W)      */
+  SLORR_OP_GRAM_REDUCE = 10 /* sum of split-K Gram partials, A = X X^T    */
 } slorr_op_t;
 
 /* Measurement variant of slorr_reg_fwd_bwd (same arguments and results): the
@@ -259,10 +285,6 @@ typedef struct {
   double mfma_flops;       /* flops the MFMA units execute per call (padded tiles)   */
   double weight_bytes;     /* sum_i rows_i * cols_i * sizeof(dtype)                  */
   size_t workspace_bytes;
-  int32_t gram_space;      /* matrices iterated in Gram space (P x P products, the   */
-                           /* gradient from M X_0): 0 unless SLORR_GRAM_SPACE is set; */
-                           /* then those with padded Q >= 2 P, quintic tables only    */
-  double m_scale;          /* scale of M in the iterate type                         */
 } slorr_plan_info_t;
 
 SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_t *info);
@@ -271,9 +293,8 @@ SLORR_API slorr_status_t slorr_plan_get_info(slorr_plan_t plan, slorr_plan_info_
  * slorr_plan_info_t.launches entries. ops[i] is the
  * kernel kind (slorr_op_t) of launch i; alg_flops[i] its algorithmic work:
  * the products it performs, on the unpadded shapes and counted in full
- * (2 m n k each, symmetric outputs not halved): A = X X^T 2 P^2 Q, B X and
- * the gradient product M X_0 2 P^2 Q, every P x P product (poly, Gram
- * space) 2 P^3; 0 for
+ * (2 m n k each, symmetric outputs not halved): A = X X^T and B X 2 P^2 Q,
+ * the poly's A A 2 P^3; 0 for
  * the memory-bound and reduction kernels. tile_edge[i] is the block tile edge
  * of a product launch (128 or 256: the kernel instance a profiler names), 0
  * for the others. Any of the three arrays may be NULL. Host only. */

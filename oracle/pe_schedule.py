@@ -27,8 +27,15 @@ which spans the same space as {x, x^3, x^5} but stays well conditioned when
 the interval shrinks around 1 (late steps); the returned coefficients are the
 monomial ones (a_t, b_t, c_t) of p_t(x) = a_t x + b_t x^3 + c_t x^5.
 
-Reading (paper silent): Polar Express' optional stabilisations (a safety
-factor on the polynomial, a cushioned lower bound) are not applied. Once the
+Reading (paper silent on the details): of the Polar Express stabilisations
+the paper mentions, the safety factor is applied to the default table: every
+step but the last evaluates p_t(x / 1.01) (stabilize, default_table). The
+greedy schedule maps [l, 1] onto [1 - E_1, 1 + E_1] with 1 + E_1 close to 2,
+and near the top of each interval the next polynomials are steep: without the
+factor, the rounding of a 16-bit iterate can push a singular value past the
+next interval, after which the later polynomials send it far off (a random
+7 x 13 bf16 matrix reached 27 instead of 1). The cushioned lower bound is not
+applied. pe_schedule returns the greedy rows themselves. Once the
 error E_t falls below E_STOP = 1e-4, the minimax problem on the next interval
 [1 - E_t, 1 + E_t] is no longer resolvable in float64 (its own optimal error
 is ~0.6 E_t^3 for d = 5, ~E_t^2 for d = 3, at or below the rounding of 1). From
@@ -132,6 +139,30 @@ def pe_schedule(T: int, ell: float = 1e-3, d: int = 5) -> np.ndarray:
         rows.append(coeffs)
         lo, hi = 1.0 - err, 1.0 + err
     return np.array(rows, dtype=np.float64)
+
+
+DEFAULT_SAFETY = 0.01
+
+
+def stabilize(table, delta: float = DEFAULT_SAFETY) -> np.ndarray:
+    """The schedule with the numerical stabilisation applied (the reading taken
+    of the paper's unspecified stabilisations of Polar Express): every step but
+    the last evaluates its polynomial at x / (1 + delta),
+        p_t(x / s) = (a_t / s) x + (b_t / s^3) x^3 + (c_t / s^5) x^5,  s = 1 + delta,
+    so that a singular value pushed slightly above the step's interval by the
+    rounding of a low-precision iterate is mapped back inside the next one
+    instead of off the polynomial's controlled range."""
+    t = np.array(table, dtype=np.float64, copy=True)
+    s = 1.0 + float(delta)
+    t[:-1, 0] /= s
+    t[:-1, 1] /= s ** 3
+    t[:-1, 2] /= s ** 5
+    return t
+
+
+def default_table(T: int, ell: float = 1e-3, d: int = 5, delta: float = DEFAULT_SAFETY) -> np.ndarray:
+    """The default coefficient table: the first T greedy rows, stabilised."""
+    return stabilize(pe_schedule(T, ell, d), delta)
 
 
 def apply_scalar(table: np.ndarray, x: np.ndarray) -> np.ndarray:

@@ -18,11 +18,12 @@ widened exactly from its storage type to float64):
                                                  + c_t (XX^T)^2 X
   O5  P = X_T, transposed back when M > N: the approximate polar factor U V^T
   O6  n = sum(W * P)            (Sec. 3: sum(W . UV^T) = tr(Sigma) = ||W||_*)
-  O7  Hoyer:   r = n / f_eps,  L = r^2,
-               grad = g * 2 r * (P / f_eps - n / f_eps^3 * W)
-                                 (Eq. SLORR_grads with U V^T -> P and
-                                  ||W||_F -> ||W||_F + eps, as in Listing 1;
-                                  no differentiation through O4, Sec. 3)
+  O7  Hoyer:   L = (n / f_eps)^2; Eq. SLORR_grads, d(||W||_*^2 / ||W||_F^2)/dW
+               = (2 n / f^2) U V^T - (2 n^2 / f^4) W, with U V^T -> P and
+               f -> f_eps (the substitution Listing 1 makes):
+                 grad = g * (s1 * P - s2 * W),  s1 = 2 n / f_eps^2,
+                                                s2 = 2 n^2 / f_eps^4
+               (no differentiation through O4, Sec. 3)
       Nuclear: L = n,  grad = g * P      (Eq. SLORR_grads, right part)
   O8  set value = sum_i L_i     (Sec. 3, definition of L_hoyer and L_nuc)
 
@@ -88,7 +89,9 @@ def fwd_bwd(W, kind: str, table, eps: float = 0.0, g: float = 1.0) -> OracleResu
     if kind == HOYER:                                     # O7
         r = n_hat / f_eps
         value = r * r
-        grad = g * 2.0 * r * (P / f_eps - (n_hat / f_eps ** 3) * W)
+        s1 = 2.0 * n_hat / f_eps ** 2
+        s2 = 2.0 * n_hat ** 2 / f_eps ** 4
+        grad = g * (s1 * P - s2 * W)
     else:
         r = n_hat
         value = n_hat

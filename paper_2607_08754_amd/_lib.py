@@ -9,6 +9,9 @@ import ctypes
 import os
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libslorr.so")
+# another build of the same library (e.g. the sanitizer build of the CPU tests)
+if os.environ.get("SLORR_LIB"):
+    LIB_PATH = os.environ["SLORR_LIB"]
 
 # status codes
 OK = 0
@@ -27,12 +30,11 @@ VALUES_ONLY = 0x2
 NO_GRAPH = 0x4
 AUX = 0x8
 DEFER_GRAD = 0x10
-GRAM_SPACE = 0x20
 
-OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce",
-       "grad_prod")
+OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "grad", "setsum", "gram_reduce")
 
-EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan_create",
+EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan", "slorr_cache_config",
+            "slorr_cache_clear",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",
             "slorr_reg_fwd_bwd_profiled",
             "slorr_plan_destroy", "slorr_plan_get_info", "slorr_plan_get_launches", "slorr_status_string",
@@ -46,15 +48,14 @@ class Shape(ctypes.Structure):
 class Options(ctypes.Structure):
     _fields_ = [("iters", ctypes.c_int32), ("degree", ctypes.c_int32), ("ell", ctypes.c_double),
                 ("coeffs", ctypes.POINTER(ctypes.c_double)), ("eps", ctypes.c_float),
-                ("flags", ctypes.c_uint32), ("grad_dtype", ctypes.c_int)]
+                ("flags", ctypes.c_uint32), ("grad_dtype", ctypes.c_int), ("safety", ctypes.c_double)]
 
 
 class PlanInfo(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("groups", ctypes.c_int32), ("iters", ctypes.c_int32),
                 ("launches", ctypes.c_int32), ("gemm_tiles", ctypes.c_int64),
                 ("paper_flops", ctypes.c_double), ("mfma_flops", ctypes.c_double),
-                ("weight_bytes", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t),
-                ("gram_space", ctypes.c_int32), ("m_scale", ctypes.c_double)]
+                ("weight_bytes", ctypes.c_double), ("workspace_bytes", ctypes.c_size_t)]
 
 
 class SlorrError(RuntimeError):
@@ -83,9 +84,13 @@ def lib() -> ctypes.CDLL:
         L.slorr_default_options.restype = None
         L.slorr_pe_coefficients.argtypes = [ctypes.c_double, i32, i32, ctypes.POINTER(ctypes.c_double)]
         L.slorr_pe_coefficients.restype = ctypes.c_int
-        L.slorr_plan_create.argtypes = [ctypes.POINTER(vp), i32, ctypes.POINTER(Shape), ctypes.c_int,
-                                        ctypes.c_int, ctypes.POINTER(Options), ctypes.POINTER(sz)]
-        L.slorr_plan_create.restype = ctypes.c_int
+        L.slorr_plan.argtypes = [ctypes.POINTER(vp), i32, ctypes.POINTER(Shape), ctypes.c_int,
+                                 ctypes.c_int, ctypes.POINTER(Options), ctypes.POINTER(sz)]
+        L.slorr_plan.restype = ctypes.c_int
+        L.slorr_cache_config.argtypes = [ctypes.c_int, ctypes.POINTER(Options)]
+        L.slorr_cache_config.restype = None
+        L.slorr_cache_clear.argtypes = []
+        L.slorr_cache_clear.restype = ctypes.c_int
         L.slorr_plan_set_workspace.argtypes = [vp, vp, sz]
         L.slorr_plan_set_workspace.restype = ctypes.c_int
         L.slorr_reg_fwd_bwd.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape), ctypes.c_int,

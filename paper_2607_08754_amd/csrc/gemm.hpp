@@ -14,8 +14,13 @@
 //                                      Cubic steps (no Poly) use X' = a X + b A X
 //                                      with the a X term in the epilogue.
 //   Last    X_T = B X, stored like an update, with the per-tile partial
-//           sums of W * P (P = X_T in fp32; the trace of W^T P) read against W
-//           in its own orientation
+//           sums of X_0' * P over the canonical tile: P = X_T as stored
+//           (rounded to the iterate type, the values the gradient kernel
+//           reads) and X_0' = W / 2^e, which holds W's values exactly, so
+//           that 2^e times the sum is the trace sum(W * P) of Sec. 3
+//
+// The first step runs on X_0' = W / 2^e and applies kappa = 2^e / (f + eps)
+// through its coefficients (per matrix: kappa a, kappa^3 b, kappa^5 c).
 //
 // Gram and Poly outputs are symmetric: only tiles with tm <= tn are computed
 // and off-diagonal tiles are also stored transposed (mirror).
@@ -57,10 +62,7 @@ template <> struct Mfma<float> {
   }
 };
 
-// kGrad / kGradB: the Gram-space gradient, g (s1 P - s2 W) with P = M X_0
-// formed tile by tile and written straight into the caller's fp32 / bf16
-// gradient (W's orientation)
-enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2, kLast = 3, kGrad = 4, kGradB = 5 };
+enum GemmMode { kGram = 0, kPoly = 1, kUpdate = 2, kLast = 3 };
 
 struct GemmArgs {
   const Tile *tiles;
@@ -68,24 +70,14 @@ struct GemmArgs {
   const DynDesc *dyn;
   char *ws;
   double *tpart;
-  int which_x;    // current X buffer
-  int use_a;      // update operand is A (cubic step)
-  int use_m;      // the A operand is M (Gram-space gradient product M X_0)
-  int which_m;    // M buffer: written by a B M product, read by M X_0
-  int which_b;    // B buffer: b (0) or b1 (1)
-  int m_from_b;   // M = B M_prev reads M_prev = B_0 from b
-  int store_a0;   // first Gram: also store A_0 for Gram-space matrices
-  int trace_m;    // M = B M_prev: per-tile partials of (f + eps) tr(M A_0) * tscale
-  float tscale;
   const Scalars *sc;
+  int xin, xout;  // X buffers read / written (MatDesc::x index)
+  int use_a;      // update operand is A (cubic step)
   int write_x;    // Last: store X_T (the gradient kernel reads it)
   int fold;       // Update / Last: a_t I is folded into the operand (no a X term)
+  int kap;        // first step: coefficients times powers of the matrix's kappa
   float alpha, beta, gamma, inv_sx;
-  float alpha2;   // scale of the Gram-space A = B C and M = B M_prev
-  float mscale;   // gradient product: scale of M
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
-  const CallParams *call;   // Grad: upstream factors
-  int accumulate; // Grad: add into the gradient buffers
 };
 
 template <int BM, int BN, int WGM, int WGN>
@@ -161,94 +153,6 @@ __device__ __forceinline__ void lds_dma_wait() {
   asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
 #endif
 }
-
-// Gradient run of nv elements at g from t = s1 P - s2 W: u = fl(gsc t) (u
-// rounded to bf16 for bf16 buffers), then g = fl(g + u) when accumulating; no
-// contraction, the rounding the gradient kernel uses. Whole runs are stored
-// non-temporally (the gradient is not read again in the call).
-template <typename Tg>
-__device__ __forceinline__ void grad8(Tg *g, int nv, const float (&t)[8], float gsc, int accumulate) {
-#pragma clang fp contract(off)
-  float v[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    v[j] = gsc * t[j];
-    if constexpr (sizeof(Tg) == 2) v[j] = to_f(from_f<Tg>(v[j]));
-  }
-  if (accumulate) {
-    float old[8];
-    get8(g, nv, old);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = old[j] + v[j];
-  }
-  if (nv == 8 && (reinterpret_cast<uintptr_t>(g) & 15) == 0) {
-    if constexpr (sizeof(Tg) == 2) {
-      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-      u16x8 h;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) h[j] = from_f<Tg>(v[j]);
-      __builtin_nontemporal_store(h, reinterpret_cast<u16x8 *>(g));
-    } else {
-      float4v a, b;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        a[j] = v[j];
-        b[j] = v[4 + j];
-      }
-      __builtin_nontemporal_store(a, reinterpret_cast<float4v *>(g));
-      __builtin_nontemporal_store(b, reinterpret_cast<float4v *>(g) + 1);
-    }
-  } else {
-    put8(g, nv, v);
-  }
-}
-
-// sum_j v[j] * w[j] over the first n (<= 8) entries of w (global memory).
-template <typename Tw>
-__device__ __forceinline__ double dot_w(const Tw *w, const float (&v)[8], int n) {
-  float wv[8];
-  if (n == 8 && (reinterpret_cast<uintptr_t>(w) & 15) == 0) {
-    if constexpr (sizeof(Tw) == 2) {
-      typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-      const u16x8 h = *reinterpret_cast<const u16x8 *>(w);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) wv[j] = to_f(Tw(h[j]));
-    } else {
-      const float4v a = reinterpret_cast<const float4v *>(w)[0];
-      const float4v b = reinterpret_cast<const float4v *>(w)[1];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        wv[j] = a[j];
-        wv[4 + j] = b[j];
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) wv[j] = j < n ? to_f(w[j]) : 0.0f;
-  }
-  double s = 0.0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wv[j]);
-  return s;
-}
-
-// 8 consecutive weights as loaded (bf16 bits or fp32), for a load issued
-// ahead of its use.
-template <typename Tw> struct WChunk;
-template <> struct WChunk<uint16_t> {
-  typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
-  u16x8 h;
-  __device__ __forceinline__ void load(const uint16_t *p) { h = *reinterpret_cast<const u16x8 *>(p); }
-  __device__ __forceinline__ float get(int j) const { return __uint_as_float(uint32_t(h[j]) << 16); }
-};
-template <> struct WChunk<float> {
-  float4v a, b;
-  __device__ __forceinline__ void load(const float *p) {
-    a = reinterpret_cast<const float4v *>(p)[0];
-    b = reinterpret_cast<const float4v *>(p)[1];
-  }
-  __device__ __forceinline__ float get(int j) const { return j < 4 ? a[j] : b[j - 4]; }
-};
 
 // 8 consecutive iterate values (fp16 or fp32) as loaded, for a load issued
 // ahead of its use.
@@ -338,6 +242,14 @@ __device__ __forceinline__ void store8_range(T *p, const float (&v)[8], int lo, 
     if (j >= lo && j < hi) p[j] = T(v[j]);
 }
 
+// The value the iterate buffer holds for an fp32 result v (the rounding of
+// the store), as a float.
+template <typename T>
+__device__ __forceinline__ float as_stored(float v) {
+  if constexpr (sizeof(T) == 2) return float(_Float16(v));
+  return v;
+}
+
 template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   using S = GemmShape<BM, BN, WGM, WGN>;
@@ -345,8 +257,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int V = Mfma<T>::V;
   constexpr int BK = 8 * V;                      // k per slab (128-byte rows)
   constexpr int FM = S::FM, FN = S::FN, WTM = S::WTM, WTN = S::WTN;
-  constexpr bool GR = MODE == kGrad || MODE == kGradB;
-  constexpr bool KN = (MODE == kUpdate || MODE == kLast || GR);
+  constexpr bool KN = (MODE == kUpdate || MODE == kLast);
   // fp16 [k][n] operand: global -> LDS directly in its own layout, transposed
   // on the LDS read; fp32 goes through registers and is stored transposed
   constexpr bool TR = KN && sizeof(T) == 2;
@@ -365,39 +276,30 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const bool part = MODE == kGram && tile.k1 > 0;
   // diagonal tile of a product of a matrix with itself (X X^T, A A; BM == BN):
   // the A and B operands are the same row panel, loaded once and read for both
-  const bool diag = (MODE == kGram || MODE == kPoly) && tile.op == 0 && BM == BN && tile.tm == tile.tn;
+  const bool diag = (MODE == kGram || MODE == kPoly) && BM == BN && tile.tm == tile.tn;
   const MatDesc d = args.mats[tile.mat];
   const int m0 = tile.tm * BM, n0 = tile.tn * BN;
-  T *Xc = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x1 : d.x0));
-  T *Xn = reinterpret_cast<T *>(args.ws + (args.which_x ? d.x0 : d.x1));
+  // X buffer offsets read from the table in memory (a run-time index into the
+  // local copy of the descriptor would place that copy in scratch memory)
+  T *Xc = reinterpret_cast<T *>(args.ws + args.mats[tile.mat].x[args.xin]);
+  T *Xn = reinterpret_cast<T *>(args.ws + args.mats[tile.mat].x[args.xout]);
   T *Am = reinterpret_cast<T *>(args.ws + d.a);
-  T *Bm = reinterpret_cast<T *>(args.ws + (args.which_b ? d.b1 : d.b));
-  T *Cm = reinterpret_cast<T *>(args.ws + d.c);
-  T *Mw = reinterpret_cast<T *>(args.ws + (args.which_m ? d.m1 : d.m0));   // M written / read
-  T *Mr = reinterpret_cast<T *>(args.ws + (args.m_from_b ? d.b : args.which_m ? d.m0 : d.m1));   // M_prev of B M
+  T *Bm = reinterpret_cast<T *>(args.ws + d.b);
 
   const T *Ap;
   const T *Bp;
   int lda, ldb, K;
-  // the symmetric-output products, by tile.op (every operand but X is
-  // symmetric, so B Y = B Y^T is an NT product of rows)
-  if (MODE == kGram && tile.op == kOpXX) {          // A = X X^T
+  if (MODE == kGram) {                               // A = X X^T
     Ap = Xc; Bp = Xc; lda = ldb = d.Qp; K = d.Qp;
     if (part) {
       Ap += tile.k0;
       Bp += tile.k0;
       K = tile.k1 - tile.k0;
     }
-  } else if (MODE == kGram) {                        // A = B C (Gram space)
-    Ap = Bm; Bp = Cm; lda = ldb = d.Pp; K = d.Pp;
   } else if (MODE == kPoly) {                        // A A
     Ap = Am; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
-  } else if (tile.op == kOpBM) {                     // M = B M_prev (Gram space)
-    Ap = Bm; Bp = Mr; lda = ldb = d.Pp; K = d.Pp;
-  } else if (tile.op == kOpBA) {                     // C = B A (Gram space)
-    Ap = Bm; Bp = Am; lda = ldb = d.Pp; K = d.Pp;
-  } else {                                           // B X, A X, or M X_0
-    Ap = args.use_m ? Mw : (args.use_a ? Am : Bm); Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
+  } else {                                           // B X or A X
+    Ap = args.use_a ? Am : Bm; Bp = Xc; lda = d.Pp; ldb = d.Qp; K = d.Pp;
   }
 
   const int tid = threadIdx.x;
@@ -522,29 +424,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // K is a multiple of 128 (padding) and BK divides it. One LDS stage is
   // multiplied while the other is filled by direct loads (and the transposed
   // update operand) for the next slab.
-  // Grad: the product runs on M - r I, r = s2 (f + eps) / s1, so that it
-  // gives s1 (M - r I) X_0 = s1 P - s2 W (W = (f + eps) X_0) and the epilogue
-  // reads no W: where a k-slab crosses the tile's rows, the diagonal entries
-  // of M in the published LDS stage are shifted (then a barrier) before the
-  // slab's MFMAs read them.
-  float shift = 0.0f;
-  if constexpr (GR) {
-    const Scalars sv = args.sc[tile.mat];
-    if (sv.s1 != 0.0) shift = float(sv.s2 * sv.feps / sv.s1 * double(args.mscale));
-  }
-  auto dshift = [&](int kt, int buf) {
-    if constexpr (GR) {
-      const int k0 = kt * BK, lo = max(k0, m0), hi = min(k0 + BK, m0 + BM);
-      if (shift != 0.0f && lo < hi) {              // uniform over the block
-        if (tid < hi - lo) {
-          const int m = lo + tid, r = m - m0, kk = m - k0;
-          T *e = reinterpret_cast<T *>(smem + buf * S::kStage + swz(r, kk / V)) + kk % V;
-          *e = T(float(*e) - shift);
-        }
-        __syncthreads();
-      }
-    }
-  };
   const int nk = K / BK;
   dload(0, 0);
   kload(0);
@@ -557,7 +436,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       dload((kt + 1) * BK, nb);
       kload((kt + 1) * BK);
     }
-    dshift(kt, kt & 1);
     compute(kt & 1);
     if (kt + 1 < nk) kstore(nb);
     lds_dma_wait();
@@ -568,105 +446,59 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   // acc[i][j][r] holds row 8 (r / 4) + 4 lk + r % 4 and column lr of MFMA tile
   // (i, j). Per 32-row block of the wave tile: stage in the wave's own LDS
   // area (fp32), then finish row-wise with 16-byte accesses, then (mirror
-  // tiles, tall P) write the transpose column-wise. The waves do not wait for
-  // each other during the epilogue.
+  // tiles) write the transpose column-wise. The waves do not wait for each
+  // other during the epilogue.
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
-  // Gram-space A = B C and M = B M_prev scale by alpha2; the poly adds b A + a I
-  const bool gsp = (MODE == kGram && tile.op == kOpBC) || (KN && tile.op == kOpBM);
-  const float alpha = gsp ? args.alpha2 : args.alpha, beta = args.beta;
+  // per-matrix coefficients of the first step (kappa = 2^e / (f + eps))
+  float alpha = args.alpha, beta = args.beta, gamma = args.gamma;
+  if (args.kap) {
+    const double kp = args.sc[tile.mat].kappa, k2 = kp * kp;
+    if (MODE == kPoly) {
+      alpha = float(double(args.alpha) * k2 * k2 * kp);
+      beta = float(double(args.beta) * k2 * kp);
+      gamma = float(double(args.gamma) * kp);
+    } else {
+      alpha = float(double(args.alpha) * k2 * kp);
+      beta = float(double(args.beta) * kp);
+    }
+  }
   // symmetric output and where it goes
-  T *Sym = MODE == kGram ? Am : (MODE == kPoly ? Bm : Cm);
-  const bool store_a0 = MODE == kGram && tile.op == kOpXX && args.store_a0 && d.gs;
-  // the last M = B M_prev of a Gram-space matrix (in the last step's launch,
-  // beside the X-space last updates): trace partials against A_0
-  const bool mtrace = MODE == kLast && tile.op == kOpBM && args.trace_m;
-  // an X-space last update: P and its trace against W
-  const bool xlast = MODE == kLast && tile.op == kOpBX;
+  T *Sym = MODE == kGram ? Am : Bm;
   // Symmetric outputs are stored exactly symmetric: off-diagonal tiles also
   // store their transpose; a diagonal tile stores its upper triangle and the
   // transpose of it below the diagonal (its own lower triangle, computed with
-  // a different rounding, is not used). The Gram-space products need this:
-  // with operands symmetric only up to rounding, B Y^T (the NT product) and
-  // B Y drift apart over the steps.
-  const bool mirror = ((MODE == kGram || MODE == kPoly) && !part) || (MODE == kUpdate && tile.op == kOpBA);
+  // a different rounding, is not used).
+  const bool mirror = (MODE == kGram || MODE == kPoly) && !part;
   const bool dtile = mirror && tile.tm == tile.tn;
-  constexpr bool WR = MODE == kLast || GR;    // the epilogue reads W or writes in its layout
-  const bool colwise = mirror || (xlast && d.tall);
   double tsum = 0.0;
-  const Tw *W = WR ? static_cast<const Tw *>(args.dyn[tile.mat].w) : nullptr;
 
-  // Last: the weights each lane multiplies into the trace are known before
-  // the accumulators are staged, so they are loaded one 32-row block ahead
-  // (two register buffers) instead of being waited for task by task. Task t
-  // of a lane: row phase (wide W) row / column group, column phase (tall W)
-  // row group / column; both phases have NTASK tasks per lane.
+  // Poly: the A values of the b A term; Last: the X_0' values of the trace.
+  // Loaded one 32-row block ahead (two register buffers). Task t of a lane:
+  // row task / CG, 8 columns from (task % CG) 8 of the staged block.
   constexpr int NTASK = 32 * CG / 64;
-  static_assert(NTASK * 64 == 32 * CG && NTASK * 64 == WTN * 4, "epilogue task split");
-  WChunk<Tw> wpre[2][NTASK];
-  bool wfull[2][NTASK];
-  auto wtask = [&](int i, int t, const Tw *&ptr, int &nv) -> bool {
-    const int task = lane + 64 * t;
-    const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
-    if (!d.tall) {                     // canonical (m, n) = W[m][n]
-      const int grow = grow0 + task / CG, gcol = gcol0 + (task % CG) * 8;
-      ptr = W + size_t(grow) * d.cols + gcol;
-      nv = min(8, d.Q - gcol);
-      return grow < d.P && gcol < d.Q;
-    }
-    const int orow = gcol0 + (task >> 2), ocol = grow0 + (task & 3) * 8;   // W[n][m]
-    ptr = W + size_t(orow) * d.cols + ocol;
-    nv = min(8, d.P - ocol);
-    return orow < d.Q && ocol < d.P;
-  };
-  auto wprefetch = [&](int i, int b) {
-#pragma unroll
-    for (int t = 0; t < NTASK; ++t) {
-      const Tw *ptr;
-      int nv;
-      const bool ok = wtask(i, t, ptr, nv);
-      wfull[b][t] = ok && nv == 8 && (reinterpret_cast<uintptr_t>(ptr) & 15) == 0;
-      if (wfull[b][t]) wpre[b][t].load(ptr);
-    }
-  };
-  // sum_j v[j] * W(task)[j] for task t of block i (prefetched or direct)
-  auto wdot = [&](int i, int b, int t, const float (&v)[8]) -> double {
-    const Tw *ptr;
-    int nv;
-    if (!wtask(i, t, ptr, nv)) return 0.0;
-    if (!wfull[b][t]) return dot_w(ptr, v, nv);
-    double s = 0.0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) s += double(v[j]) * double(wpre[b][t].get(j));
-    return s;
-  };
-  if constexpr (MODE == kLast)
-    if (xlast) wprefetch(0, 0);
-  // Poly: the A values of the b A term, likewise one 32-row block ahead; the
-  // last M product of a Gram-space matrix: the A_0 values of its trace
-  XChunk<T> apre[2][NTASK];
-  // (fp32 iterate: the last step's launch, which also prefetches W for its
-  // X-space tiles, reads A_0 when it uses it: registers)
-  const bool apref = MODE == kPoly || (mtrace && sizeof(T) == 2);
-  const T *asrc = mtrace ? reinterpret_cast<const T *>(args.ws + d.a0) : Am;
+  static_assert(NTASK * 64 == 32 * CG, "epilogue task split");
+  // fp32 iterate in the last step: no prefetch (registers), X_0' is loaded
+  // where it is used
+  constexpr bool APRE = MODE == kPoly || (MODE == kLast && sizeof(T) == 2);
+  XChunk<T> apre[APRE ? 2 : 1][NTASK];
+  const T *asrc = MODE == kLast ? reinterpret_cast<const T *>(args.ws + d.x[0]) : Am;
+  const int apitch = MODE == kLast ? d.Qp : d.Pp;
   auto aprefetch = [&](int i, int b) {
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
 #pragma unroll
     for (int t = 0; t < NTASK; ++t) {
       const int task = lane + 64 * t;
-      apre[b][t].load(asrc + size_t(grow0 + task / CG) * d.Pp + gcol0 + (task % CG) * 8);
+      apre[b][t].load(asrc + size_t(grow0 + task / CG) * apitch + gcol0 + (task % CG) * 8);
     }
   };
-  if constexpr (MODE == kPoly || MODE == kLast)
-    if (apref) aprefetch(0, 0);
+  if constexpr (APRE) aprefetch(0, 0);
 
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
-    if constexpr (MODE == kLast)
-      if (i + 1 < FM && xlast) wprefetch(i + 1, (i + 1) & 1);
-    if constexpr (MODE == kPoly || MODE == kLast)
-      if (i + 1 < FM && apref) aprefetch(i + 1, (i + 1) & 1);
+    if constexpr (APRE)
+      if (i + 1 < FM) aprefetch(i + 1, (i + 1) & 1);
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -675,42 +507,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     // performed in order: a wave-level barrier (no reordering) suffices
     __builtin_amdgcn_wave_barrier();
     const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
-    if constexpr (GR) {
-      // g s1 (P - r X_0) = g (s1 P - s2 W) straight from the staged block, in
-      // W's orientation: runs of 8 along W's rows (canonical rows of a wide W,
-      // canonical columns of a tall one), the tasks of wtask
-      typedef typename std::conditional<MODE == kGradB, bf16_t, float>::type Tg;
-      Tg *G = static_cast<Tg *>(args.dyn[tile.mat].g);
-      const float s1 = float(args.sc[tile.mat].s1) * args.inv_sx;
-      const float gsc = args.call->gscale ? args.call->grad_scale * args.call->gscale[tile.mat]
-                                          : args.call->grad_scale;
-#pragma unroll
-      for (int t = 0; t < NTASK; ++t) {
-        const int task = lane + 64 * t;
-        const Tw *ptr;
-        int nv;
-        if (!wtask(i, t, ptr, nv)) continue;
-        float v[8];
-        if (!d.tall) {
-          const float4v *e = reinterpret_cast<const float4v *>(ep + (task / CG) * P + (task % CG) * 8);
-          const float4v e0 = e[0], e1 = e[1];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            v[j] = e0[j] * alpha;
-            v[4 + j] = e1[j] * alpha;
-          }
-        } else {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] = ep[((task & 3) * 8 + j) * P + (task >> 2)] * alpha;
-        }
-        float tv[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) tv[j] = s1 * v[j];
-        grad8(G + (ptr - W), nv, tv, gsc, args.accumulate);
-      }
-      __builtin_amdgcn_wave_barrier();
-      continue;
-    }
 #pragma unroll
     for (int t = 0; t < NTASK; ++t) {
       const int task = lane + 64 * t;
@@ -733,14 +529,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] *= alpha;
           store8_range(Sym + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
-          if (store_a0)
-            store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(grow) * d.Pp + gcol, v,
-                         dtile ? grow - gcol : 0, 8);
         }
       } else if (MODE == kPoly) {
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? args.gamma : 0.0f);
+          v[j] = beta * apre[i & 1][t].get(j) + alpha * v[j] + (grow == gcol + j ? gamma : 0.0f);
         const int lo = dtile ? grow - gcol : 0;
         store8_range(Sym + size_t(grow) * d.Pp + gcol, v, lo, 8);
       } else {
@@ -753,31 +546,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) v[j] = beta * in[j] + alpha * v[j];
         }
-        if ((MODE == kUpdate || MODE == kLast) && tile.op == kOpBM) {
-          store8_stream(Mw + size_t(grow) * d.Pp + gcol, v);
-          if (mtrace) {
-            if constexpr (sizeof(T) == 2) {
+        if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
+        if (MODE == kLast) {
+          // P as stored times X_0' (both in the iterate's scale): the products
+          // of two fp16 (or fp32) values are exact in fp64
 #pragma unroll
-              for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(apre[i & 1][t].get(j));
+          for (int j = 0; j < 8; ++j) {
+            float x0;
+            if constexpr (APRE) {
+              x0 = apre[i & 1][t].get(j);
             } else {
-              XChunk<T> a0;
-              a0.load(asrc + size_t(grow) * d.Pp + gcol);
-#pragma unroll
-              for (int j = 0; j < 8; ++j) tsum += double(v[j]) * double(a0.get(j));
+              x0 = float(asrc[size_t(grow) * apitch + gcol + j]);
             }
+            tsum += double(as_stored<T>(v[j])) * double(x0);
           }
-        } else if (MODE == kUpdate && tile.op == kOpBA) {
-          store8_range(Cm + size_t(grow) * d.Pp + gcol, v, dtile ? grow - gcol : 0, 8);
-        } else if (MODE == kUpdate || (MODE == kLast && args.write_x)) {
-          store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
-        }
-        if (xlast) {
-#pragma unroll
-          for (int j = 0; j < 8; ++j) v[j] *= args.inv_sx;     // P in its own scale
-          if (!d.tall) tsum += wdot(i, i & 1, t, v);
         }
       }
-      if (colwise) {
+      if (mirror) {
         float4v e0, e1;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -789,7 +574,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       }
     }
     __builtin_amdgcn_wave_barrier();
-    if (colwise) {
+    if (mirror) {
       // transpose: output row = this tile's column, 8 consecutive source rows
 #pragma unroll
       for (int t = 0; t < NTASK; ++t) {
@@ -799,20 +584,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = ep[(rg * 8 + j) * P + col];
         const int orow = gcol0 + col, ocol = grow0 + rg * 8;
-        if (MODE == kGram || MODE == kPoly || MODE == kUpdate) {
-          const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
-          store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
-          if (store_a0) store8_range(reinterpret_cast<T *>(args.ws + d.a0) + size_t(orow) * d.Pp + ocol, v, 0, hi);
-        } else if (MODE == kLast) {
-          tsum += wdot(i, i & 1, t, v);       // tall W (colwise only for tall)
-        }
+        const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
+        store8_range(Sym + size_t(orow) * d.Pp + ocol, v, 0, hi);
       }
       __builtin_amdgcn_wave_barrier();
     }
   }
-  if (MODE == kLast || mtrace) {
+  if (MODE == kLast) {
     __syncthreads();                      // the block sum reuses wave 0's staging area
     const double r = block_sum<NT>(tsum, reinterpret_cast<double *>(smem));
-    if (tid == 0) args.tpart[tile.slot] = mtrace ? r * args.sc[tile.mat].feps * double(args.tscale) : r;
+    if (tid == 0) args.tpart[tile.slot] = r;
   }
 }

@@ -2,13 +2,17 @@
 //
 //   k_sumsq    sum of squares of W per chunk (a2: ||W||_F, Sec. 3), fp64
 //              accumulation, wave shuffle + LDS reduction, fixed order
-//   k_norm_fin f = sqrt(sum), f + eps per matrix (Listing 1)
-//   k_prep     X_0 = W / (f + eps) in the canonical (short-side) orientation,
-//              zero padded, in the iterate type (Sec. 3 "Computing the polar
-//              factor"; App. D remark on normalisation)
+//   k_norm_fin f = sqrt(sum), f + eps per matrix (Listing 1), and the split of
+//              1 / (f + eps) into an exact power of two and kappa in [1, 2)
+//   k_prep     X_0' = W / 2^e in the canonical (short-side) orientation, zero
+//              padded, in the iterate type; X_0 = W / (f + eps) = kappa X_0'
+//              with kappa applied by the first step's coefficients (Sec. 3
+//              "Computing the polar factor"; App. D remark on normalisation)
 //   k_gemm     the Polar Express step (Sec. 3; App. E.1) as three MFMA GEMMs:
 //                Gram    A = X X^T
 //                Poly    B = b A + c A A + a I      (A symmetric: A A = A A^T)
+//                                                   (first step: kappa a, kappa^3 b,
+//                                                   kappa^5 c)
 //                Update  X' = B X                   (B symmetric)
 //                Last    X_T = a X + B X with the trace partials of
 //                        sum(W * P), P = X_T (Sec. 3 "Computing the nuclear
@@ -147,93 +151,14 @@ __device__ __forceinline__ void put8(T *p, int n, const float (&v)[8]) {
 
 // --------------------------------------------------------------- reductions
 
-template <typename Tw>
-__global__ __launch_bounds__(kThreads) void k_sumsq(const Chunk *__restrict__ chunks,
-                                                    const DynDesc *__restrict__ dyn,
-                                                    double *__restrict__ part) {
-  __shared__ double sh[4];
-  const Chunk ch = chunks[blockIdx.x];
-  const Tw *w = static_cast<const Tw *>(dyn[ch.mat].w) + ch.begin;
-  constexpr int V = 16 / sizeof(Tw);
-  typedef Tw vec_t __attribute__((ext_vector_type(V)));
-  double acc = 0.0;
-  if (ch.len == kChunk) {
-    // full chunk: the thread's loads are issued in batches of 8
-    constexpr int PER = kChunk / V / kThreads, BATCH = 8;
-    static_assert(PER * V * kThreads == kChunk && PER % BATCH == 0, "chunk / block mismatch");
-#pragma unroll
-    for (int k0 = 0; k0 < PER; k0 += BATCH) {
-      vec_t v[BATCH];
-#pragma unroll
-      for (int k = 0; k < BATCH; ++k)
-        v[k] = reinterpret_cast<const vec_t *>(w)[threadIdx.x + (k0 + k) * kThreads];
-#pragma unroll
-      for (int k = 0; k < BATCH; ++k)
-#pragma unroll
-        for (int j = 0; j < V; ++j) {
-          const double x = to_f(v[k][j]);
-          acc += x * x;
-        }
-    }
-  } else {
-    const int nvec = ch.len / V;
-    for (int i = threadIdx.x; i < nvec; i += kThreads) {
-      const vec_t v = reinterpret_cast<const vec_t *>(w)[i];
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const double x = to_f(v[j]);
-        acc += x * x;
-      }
-    }
-    for (int i = nvec * V + threadIdx.x; i < ch.len; i += kThreads) {
-      const double x = to_f(w[i]);
-      acc += x * x;
-    }
-  }
-  const double r = block_sum<kThreads>(acc, sh);
-  if (threadIdx.x == 0) part[blockIdx.x] = r;
-}
-
-// f and f + eps per matrix: one wave per matrix sums its chunk partials
-// (lane-strided, then a fixed butterfly).
-__global__ __launch_bounds__(kThreads) void k_norm_fin(const MatDesc *__restrict__ mats,
-                                                       Scalars *__restrict__ sc,
-                                                       const double *__restrict__ part, int n,
-                                                       float eps) {
-  const int i = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (i >= n) return;
-  const MatDesc d = mats[i];
-  double s = 0.0;
-  for (int c = d.chunk_begin + lane; c < d.chunk_end; c += 64) s += part[c];
-  s = wave_sum(s);
-  if (lane == 0) {
-    const double f = sqrt(s), fe = f + double(eps);
-    sc[i].sumsq = s;
-    sc[i].f = f;
-    sc[i].feps = fe;
-    sc[i].inv_feps = fe > 0.0 ? float(1.0 / fe) : 0.0f;
-  }
-}
-
-// ---------------------------------------------------------------- normalise
-
-// 64 x 64 canonical tile per block. Rows of W are read 8 elements at a time
-// (vector when aligned), staged in LDS as fp32, and written 8 at a time
-// along the canonical rows (transposed for tall W).
+// 64 x 64 canonical tile per block (the tiles of the normalisation), staged in
+// LDS as fp32: rows of W are read 8 elements at a time (vector when aligned).
 constexpr int kPrepPitch = kPrepTile + 4;
 
-template <typename Tw, typename Tx>
-__global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tiles,
-                                                   const MatDesc *__restrict__ mats,
-                                                   const DynDesc *__restrict__ dyn,
-                                                   const Scalars *__restrict__ sc, char *ws,
-                                                   float sx) {
-  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
-  const Tile t = tiles[blockIdx.x];
-  const MatDesc d = mats[t.mat];
-  const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
-  const float scale = sc[t.mat].inv_feps * sx;
-  Tx *x = reinterpret_cast<Tx *>(ws + d.x0);
+// Loads canonical tile t of W into LDS: tile[r * kPrepPitch + c] holds the
+// canonical element (m0 + r, n0 + c) of W (W^T for tall W), 0 outside it.
+template <typename Tw>
+__device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const MatDesc &d, const Tw *w, float scale) {
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
   // source rows of W covered by the tile: wide -> canonical rows m, tall -> canonical columns n
   const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;
@@ -243,15 +168,104 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
     float v[8];
     const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
     get8(w + size_t(r0 + r) * d.cols + c0 + c, nv, v);
+    if (d.tall) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j] * scale;
+      for (int j = 0; j < 8; ++j) tile[(c + j) * kPrepPitch + r] = v[j] * scale;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j] * scale;
+    }
   }
+}
+
+// ||W||_F^2 partial of one canonical 64 x 64 tile, fp64: thread q adds the
+// squares of canonical row q / 8, columns 8 (q % 8) .. + 7, in column order,
+// then the block sums in thread order. The order depends only on the
+// canonical tile, so W and W^T give bitwise equal partials.
+template <typename Tw>
+__global__ __launch_bounds__(kThreads) void k_sumsq(const Tile *__restrict__ tiles,
+                                                    const MatDesc *__restrict__ mats,
+                                                    const DynDesc *__restrict__ dyn,
+                                                    double *__restrict__ part) {
+  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
+  __shared__ double sh[kThreads / 64];
+  const Tile t = tiles[blockIdx.x];
+  const MatDesc d = mats[t.mat];
+  stage_tile(tile, t, d, static_cast<const Tw *>(dyn[t.mat].w), 1.0f);
+  __syncthreads();
+  double acc = 0.0;
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const double x = tile[r * kPrepPitch + c + j];
+      acc += x * x;
+    }
+  }
+  const double r = block_sum<kThreads>(acc, sh);
+  if (threadIdx.x == 0) part[t.slot] = r;
+}
+
+// f, f + eps, kappa and the X_0 scale per matrix: one wave per matrix sums its
+// chunk partials (lane-strided, then a fixed butterfly). The iterate starts
+// from X_0' = W / 2^e, 2^e the smallest power of two >= f + eps: a scaling by
+// a power of two, so X_0' holds W's values exactly (bf16 values fit fp16's
+// significand); kappa = 2^e / (f + eps) in [1, 2) goes into the first step's
+// coefficients.
+__global__ __launch_bounds__(kThreads) void k_norm_fin(const MatDesc *__restrict__ mats,
+                                                       Scalars *__restrict__ sc,
+                                                       const double *__restrict__ part, int n,
+                                                       float eps, float sx) {
+  const int i = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= n) return;
+  const MatDesc d = mats[i];
+  double s = 0.0;
+  for (int c = d.norm_begin + lane; c < d.norm_end; c += 64) s += part[c];
+  s = wave_sum(s);
+  if (lane == 0) {
+    const double f = sqrt(s), fe = f + double(eps);
+    sc[i].sumsq = s;
+    sc[i].f = f;
+    sc[i].feps = fe;
+    if (fe > 0.0 && isfinite(fe)) {
+      int e;
+      const double m = frexp(fe, &e);      // fe = m 2^e, m in [0.5, 1)
+      if (m == 0.5) --e;                   // fe is a power of two: 2^e = fe
+      sc[i].kappa = ldexp(1.0, e) / fe;
+      sc[i].two_e = ldexp(1.0, e);
+      sc[i].pscale = float(ldexp(double(sx), -e));
+    } else {
+      // zero matrix: X_0 = 0 (value and gradient 0); NaN / Inf: propagate
+      sc[i].kappa = fe > 0.0 ? 1.0 : 0.0;
+      sc[i].two_e = fe > 0.0 ? fe : 0.0;
+      sc[i].pscale = fe > 0.0 ? fe : 0.0f;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- normalise
+
+// X_0' = W / 2^e in the iterate's scale, canonical and zero padded: one 64 x 64
+// canonical tile per block, staged in LDS, written 8 elements at a time along
+// the canonical rows.
+template <typename Tw, typename Tx>
+__global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tiles,
+                                                   const MatDesc *__restrict__ mats,
+                                                   const DynDesc *__restrict__ dyn,
+                                                   const Scalars *__restrict__ sc, char *ws) {
+  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
+  const Tile t = tiles[blockIdx.x];
+  const MatDesc d = mats[t.mat];
+  // a power of two: the scaling of W is exact
+  stage_tile(tile, t, d, static_cast<const Tw *>(dyn[t.mat].w), sc[t.mat].pscale);
+  Tx *x = reinterpret_cast<Tx *>(ws + d.x[0]);
+  const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
   __syncthreads();
   for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;   // canonical (m0 + r, n0 + c..)
     float v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = d.tall ? tile[(c + j) * kPrepPitch + r] : tile[r * kPrepPitch + c + j];
+    for (int j = 0; j < 8; ++j) v[j] = tile[r * kPrepPitch + c + j];
     put8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
   }
 }
@@ -268,7 +282,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
 __global__ __launch_bounds__(64) void k_finalize(const MatDesc *__restrict__ mats, Scalars *sc,
                                                  const double *__restrict__ tpart,
                                                  const CallParams *__restrict__ call, int n, int kind,
-                                                 int aux) {
+                                                 int aux, float inv_sx) {
   const int i = blockIdx.x, lane = threadIdx.x;
   float *out = call->out_vals;
   const MatDesc d = mats[i];
@@ -276,6 +290,9 @@ __global__ __launch_bounds__(64) void k_finalize(const MatDesc *__restrict__ mat
   for (int s = d.trace_begin + lane; s < d.trace_end; s += 64) nh += tpart[s];
   nh = wave_sum(nh);
   if (lane != 0) return;
+  // the partials hold sum(X_0s * P_s) of the scaled canonical buffers:
+  // sum(W * P) = 2^e sum(X_0' * P) = 2^e / s_x^2 sum(X_0s * P_s), powers of two
+  if (!d.empty) nh *= sc[i].two_e * double(inv_sx) * double(inv_sx);
   const double fe = d.empty ? 0.0 : sc[i].feps;
   double L = 0.0, s1 = 0.0, s2 = 0.0;
   if (d.empty || fe == 0.0) {
@@ -326,16 +343,13 @@ template <typename Tx>
 __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict__ tiles,
                                                           const MatDesc *__restrict__ mats,
                                                           char *__restrict__ ws,
-                                                          const float *__restrict__ gpart, float alpha,
-                                                          int store_a0) {
+                                                          const float *__restrict__ gpart, float alpha) {
   constexpr int R = kTile / kRedStripes;          // rows per stripe
   __shared__ float t[R][kTile + 1];
   const Tile e = tiles[blockIdx.x / kRedStripes];
   const int stripe = blockIdx.x % kRedStripes;
   const MatDesc d = mats[e.mat];
   Tx *A = reinterpret_cast<Tx *>(ws + d.a);
-  Tx *A0 = reinterpret_cast<Tx *>(ws + d.a0);    // Gram space: A_0 kept for the trace
-  const bool a0 = store_a0 && d.gs;
   const int m0 = e.tm * kTile + stripe * R, n0 = e.tn * kTile;
   const float *src = gpart + size_t(e.slot) * (kTile * kTile) + stripe * R * kTile;
   for (int q = threadIdx.x; q < R * kTile / 4; q += kThreads) {
@@ -357,15 +371,13 @@ __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = t[r][c + j];
     const int lo = diag ? (m0 + r) - (n0 + c) : 0;        // upper triangle of a diagonal tile
-    for (int k = 0; k < (a0 ? 2 : 1); ++k) {
-      Tx *o = (k ? A0 : A) + size_t(m0 + r) * d.Pp + n0 + c;
-      if (lo <= 0) {
-        put8(o, 8, v);
-      } else {
+    Tx *o = A + size_t(m0 + r) * d.Pp + n0 + c;
+    if (lo <= 0) {
+      put8(o, 8, v);
+    } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (j >= lo) o[j] = from_f<Tx>(v[j]);
-      }
+      for (int j = 0; j < 8; ++j)
+        if (j >= lo) o[j] = from_f<Tx>(v[j]);
     }
   }
   // the transpose: R consecutive columns per output row (strictly below the
@@ -376,15 +388,13 @@ __global__ __launch_bounds__(kThreads) void k_gram_reduce(const Tile *__restrict
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = t[r + j][c];
     const int hi = diag ? (n0 + c) - (m0 + r) : 8;
-    for (int k = 0; k < (a0 ? 2 : 1); ++k) {
-      Tx *o = (k ? A0 : A) + size_t(n0 + c) * d.Pp + m0 + r;
-      if (hi >= 8) {
-        put8(o, 8, v);
-      } else {
+    Tx *o = A + size_t(n0 + c) * d.Pp + m0 + r;
+    if (hi >= 8) {
+      put8(o, 8, v);
+    } else {
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (j < hi) o[j] = from_f<Tx>(v[j]);
-      }
+      for (int j = 0; j < 8; ++j)
+        if (j < hi) o[j] = from_f<Tx>(v[j]);
     }
   }
 }
@@ -521,8 +531,10 @@ void go(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const Ev
 }
 
 template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
-void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev, bool grad_bf16) {
+void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
+  // the planner gives fp32 sets 128-tiles for the update launches
+  constexpr bool kUpd = sizeof(Tx) == 2 || BM == kTile;
   switch (op) {
     case Op::Gram:
       go(k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>, grid, block, s, ev, a);
@@ -531,16 +543,12 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPai
       go(k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Update:
-      go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
-      break;
-    case Op::GradProd:
-      if (grad_bf16)
-        go(k_gemm<Tx, Tw, kGradB, BM, BN, WGM, WGN>, grid, block, s, ev, a);
-      else
-        go(k_gemm<Tx, Tw, kGrad, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      if constexpr (kUpd) go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      else throw HipError("no fp32 256-tile update kernel");
       break;
     default:
-      go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      if constexpr (kUpd) go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      else throw HipError("no fp32 256-tile update kernel");
       break;
   }
 }
@@ -578,59 +586,49 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev)
     const dim3 grid(l.grid), block(kThreads);
     switch (l.op) {
       case Op::SumSq:
-        go(k_sumsq<Tw>, grid, block, s, ev, chunks, dyn, sumsq);
+        go(k_sumsq<Tw>, grid, block, s, ev, tiles + l.tile_first, mats, dyn, sumsq);
         break;
       case Op::NormFin:
-        go(k_norm_fin, grid, block, s, ev, mats, sc, sumsq, p.n, p.eps);   // 4 matrices per block
+        go(k_norm_fin, grid, block, s, ev, mats, sc, sumsq, p.n, p.eps, sx);   // 4 matrices per block
         break;
       case Op::Prep:
-        go(k_prep<Tw, Tx>, grid, block, s, ev, tiles + l.tile_first, mats, dyn, sc, ws, sx);
+        go(k_prep<Tw, Tx>, grid, block, s, ev, tiles + l.tile_first, mats, dyn, sc, ws);
         break;
       case Op::Gram:
       case Op::Poly:
       case Op::Update:
-      case Op::Last:
-      case Op::GradProd: {
+      case Op::Last: {
         GemmArgs a;
         a.tiles = tiles + l.tile_first;
         a.mats = mats;
         a.dyn = dyn;
         a.ws = ws;
         a.tpart = trace;
-        a.which_x = l.which_x;
+        a.sc = sc;
+        a.xin = l.xin;
+        a.xout = l.xout;
         a.use_a = l.use_a;
-        a.use_m = l.use_m;
-        a.which_m = l.which_m;
-        a.which_b = l.which_b;
-        a.m_from_b = l.m_from_b;
         a.write_x = (p.flags & SLORR_VALUES_ONLY) ? 0 : 1;
+        a.fold = l.fold;
+        a.kap = l.kap;
         a.alpha = l.alpha;
         a.beta = l.beta;
         a.gamma = l.gamma;
-        a.alpha2 = l.alpha2;
-        a.mscale = l.mscale;
-        a.store_a0 = l.store_a0;
-        a.trace_m = l.trace_m;
-        a.tscale = l.tscale;
-        a.sc = sc;
-        a.fold = l.fold;
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
-        a.call = call;
-        a.accumulate = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
-        const bool gb = p.grad_dtype == SLORR_BF16;
         if (l.cfg == kCfg256)
-          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev, gb);
+          launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev);
         else
-          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s, ev, gb);
+          launch_gemm<Tx, Tw, kTile, kTile, 2, 2>(l.op, grid, a, s, ev);
         break;
       }
       case Op::Finalize:
-        go(k_finalize, grid, dim3(64), s, ev, mats, sc, trace, call, p.n, int(p.kind), (p.flags & SLORR_AUX) ? 1 : 0);
+        go(k_finalize, grid, dim3(64), s, ev, mats, sc, trace, call, p.n, int(p.kind), (p.flags & SLORR_AUX) ? 1 : 0,
+           1.0f / sx);
         break;
       case Op::GramReduce:
         go(k_gram_reduce<Tx>, grid, block, s, ev, tiles + l.tile_first, mats, ws,
-           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha, l.store_a0);
+           reinterpret_cast<const float *>(ws + p.off_gpart), l.alpha);
         break;
       case Op::SetSum:
         go(k_setsum, dim3(1), dim3(1024), s, ev, sc, call, p.n);

@@ -14,7 +14,7 @@ namespace slorr {
 constexpr int kTile = 128;       // padding granularity = the small GEMM block tile
 constexpr int kBigTile = 256;    // the large GEMM block tile
 constexpr int kPrepTile = 64;    // tile of the normalise / transpose kernel
-constexpr int kChunk = 32768;    // elements per block in the norm and decoupled-update kernels
+constexpr int kChunk = 32768;    // elements per block of the decoupled-update kernel
 constexpr int kThreads = 256;    // threads per block of the non-GEMM kernels
 constexpr int kXcds = 8;         // XCDs of an MI355X; workgroup b runs on XCD b % 8
 constexpr int kCus = 256;        // compute units of an MI355X
@@ -35,15 +35,13 @@ struct MatDesc {
   int32_t P, Q, Pp, Qp;        // canonical and padded canonical shape
   int32_t tall;                // 1 if the canonical operand is W^T
   int32_t empty;               // rows == 0 or cols == 0
-  int32_t chunk_begin, chunk_end;   // slots in the norm-partials array
+  int32_t norm_begin, norm_end;     // slots in the norm-partials array (canonical tiles)
   int32_t trace_begin, trace_end;   // slots in the trace-partials array
-  int32_t gs;                  // iterated in Gram space (P x P products, gradient from M X_0)
-  int32_t pad;
-  uint64_t x0, x1, a, b;            // byte offsets in the workspace
-  uint64_t c, m0, m1;               // Gram space: C = B A and the M ping-pong
-  uint64_t b1;                      // Gram space: B of odd steps (B of even steps at b)
-  uint64_t a0;                      // Gram space: A_0 = X_0 X_0^T, kept for the trace
-  uint64_t xt;                      // X space: buffer holding X_T once the schedule has run
+  int32_t pad0, pad1;
+  uint64_t x[3];                    // byte offsets in the workspace: X_0 (kept for the
+                                    // trace), then the iterates alternate in x[1], x[2]
+  uint64_t a, b;
+  uint64_t xt;                      // buffer holding X_T once the schedule has run
 };
 
 struct DynDesc {               // per call: caller pointers
@@ -59,29 +57,30 @@ struct CallParams {            // per call
 };
 
 struct Tile {                  // one GEMM output tile / one prep tile / one Gram part
-  int32_t mat, tm, tn, slot;   // mat < 0: padding entry, the block exits at once
+  int32_t mat, tm, tn, slot;   // mat < 0: padding entry, the block exits at once;
+                               // slot: trace / norm / Gram-part partial of the tile
   int32_t k0, k1;              // Gram part: its k range [k0, k1); k1 = 0: all of K
   int32_t parts;               // Gram reduce entry: partials slot .. slot + parts - 1
-  int32_t op;                  // the tile's product (TileOp)
+  int32_t pad;
 };
-
-// Product of a GEMM tile. Gram launches (symmetric output): A = X X^T
-// (kOpXX) or, in Gram space, A = B C (kOpBC). Poly launches (symmetric
-// output): B = poly(A) (kOpPoly). Update launches: X' = B X (kOpBX) and, in
-// Gram space, M = B M_prev (kOpBM; full output, not symmetrised: B and
-// M_prev commute only up to the rounding of earlier steps) and C = B A
-// (kOpBA; symmetric output on upper tiles, A read as its own transpose, which
-// it is exactly).
-enum TileOp : int32_t { kOpXX = 0, kOpBC = 1, kOpPoly = 0, kOpBX = 0, kOpBM = 1, kOpBA = 2 };
 
 struct Chunk {                 // a contiguous run of a matrix's elements
   int32_t mat, begin, len, pad;
 };
 
-struct Scalars {               // per matrix, written by the kernels
+// Per matrix, written by the kernels. The iterate starts from the exact
+// X_0' = W / 2^e with 2^e the smallest power of two >= f + eps (a power-of-two
+// scaling, so X_0' holds W's values without rounding); the remaining factor
+// kappa = 2^e / (f + eps), in [1, 2), is applied by the first step's
+// coefficients: p_1(kappa x) = (a kappa) x + (b kappa^3) x^3 + (c kappa^5) x^5.
+struct Scalars {
   double sumsq, f, feps, nhat, value;
   double s1, s2;               // gradient = g (s1 P - s2 W)
-  float inv_feps, pad;
+  double kappa;                // 2^e / (f + eps); 0 when f + eps == 0
+  double two_e;                // 2^e: W = 2^e X_0' exactly, so the trace sum(W * P)
+                               // is 2^e sum(X_0' * P) over the canonical buffers
+  float pscale;                // 2^-e times the iterate's scale: X_0 = W pscale
+  float pad;
 };
 
 }  // namespace slorr

@@ -30,48 +30,11 @@ Tile make_tile(int32_t mat, int32_t tm, int32_t tn, int32_t slot) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// Gram-space iteration. With M_{-1} = I every iterate is X_t = M_t X_0,
-// M_t = B_t M_{t-1}, and (all B_t being polynomials of A_0 = X_0 X_0^T, so
-// that they commute) A_{t+1} = X_t X_t^T = B_t A_t B_t: the steps need only
-// P x P products (C = B A, A = B C, symmetric; M = B M) and X_T = M X_0
-// once at the end (in the gradient product): per step 8 P^3 instead of
-// 4 P^2 Q + 2 P^3 flops.
-//
-// On a singular direction with normalised value x in [0, 1] (||X_0|| <= 1)
-// the matrices act as scalars: B_t = a + b y^2 + c y^4 at y = phi_{t-1}(x),
-// M_t = prod of the B's, C_t = B_t y^2. The table's worst values over a grid
-// of x bound the entries of the stored matrices (|entry| <= spectral norm).
-// For the fp16 iterate the scale of M is the largest power of two that keeps
-// |M| * s_m <= 2^14; the Gram space is refused (false) when M, B or C would
-// not fit the type or the table is not finite.
-bool gram_space_scale(const double *coeffs, int iters, bool f16, double *scale) {
-  double mmax = 0.0, bmax = 0.0, cmax = 0.0;
-  constexpr int kGrid = 4096;
-  for (int g = 0; g <= kGrid; ++g) {
-    double y = double(g) / kGrid, m = 1.0;
-    for (int t = 0; t < iters; ++t) {
-      const double a = coeffs[3 * t], b = coeffs[3 * t + 1], c = coeffs[3 * t + 2];
-      const double y2 = y * y, bt = a + b * y2 + c * y2 * y2;
-      m *= bt;
-      bmax = std::max(bmax, std::fabs(bt));
-      cmax = std::max(cmax, std::fabs(bt) * y2);
-      mmax = std::max(mmax, std::fabs(m));
-      y *= bt;
-    }
-  }
-  if (!std::isfinite(mmax) || !std::isfinite(bmax) || !std::isfinite(cmax) || mmax <= 0.0) return false;
-  if (!f16) {
-    *scale = 1.0;
-    return mmax < 1e30;
-  }
-  constexpr double kMax = 16384.0;
-  if (bmax * kScaleB16 > kMax || cmax * kScaleA16 > kMax) return false;
-  const double s = std::exp2(std::floor(std::log2(kMax / mmax)));
-  if (!(s >= 1.0 / 64.0)) return false;      // M would lose its small entries
-  *scale = std::min(s, 1024.0);
-  return true;
-}
 int32_t round_up(int32_t x, int32_t m) { return (x + m - 1) / m * m; }
+
+// X buffer holding the iterate after t steps: X_0 stays in x[0] (the last
+// step's trace reads it), later iterates alternate between x[1] and x[2].
+int32_t xbuf(int t) { return t == 0 ? 0 : 1 + ((t - 1) & 1); }
 
 }  // namespace
 
@@ -86,15 +49,26 @@ void build_plan(Plan &p) {
   if (!(p.ell > 0.0 && p.ell < 1.0)) throw std::invalid_argument("ell must be in (0, 1)");
   if (!(p.eps >= 0.0f) || !std::isfinite(p.eps)) throw std::invalid_argument("eps must be finite and >= 0");
   if (p.flags & ~uint32_t(SLORR_ACCUMULATE | SLORR_VALUES_ONLY | SLORR_NO_GRAPH | SLORR_AUX |
-                          SLORR_DEFER_GRAD | SLORR_GRAM_SPACE))
+                          SLORR_DEFER_GRAD))
     throw std::invalid_argument("unknown flag bits");
   if ((p.flags & SLORR_VALUES_ONLY) && (p.flags & SLORR_DEFER_GRAD))
     throw std::invalid_argument("SLORR_VALUES_ONLY and SLORR_DEFER_GRAD exclude each other");
   if (p.grad_dtype != SLORR_F32 && p.grad_dtype != SLORR_BF16)
     throw std::domain_error("unsupported gradient dtype");
+  if (!(p.safety >= 0.0 && p.safety < 1.0)) throw std::invalid_argument("safety must be in [0, 1)");
   if (p.coeffs.empty()) {
+    // the built-in schedule, stabilised: every step but the last evaluates its
+    // polynomial at x / (1 + safety), i.e. (a / s, b / s^3, c / s^5), so that a
+    // singular value the iterate's rounding pushes slightly past the step's
+    // interval stays inside the next one (explicit tables are used as given)
     p.coeffs.resize(size_t(p.iters) * 3);
     greedy_schedule(p.ell, p.degree, p.iters, p.coeffs.data());
+    const double s = 1.0 + p.safety;
+    for (int t = 0; t + 1 < p.iters; ++t) {
+      p.coeffs[3 * t] /= s;
+      p.coeffs[3 * t + 1] /= s * s * s;
+      p.coeffs[3 * t + 2] /= s * s * s * s * s;
+    }
   }
   if (p.coeffs.size() != size_t(p.iters) * 3) throw std::invalid_argument("coefficient table size");
   for (double c : p.coeffs)
@@ -102,23 +76,13 @@ void build_plan(Plan &p) {
 
   const bool f16 = p.dtype == SLORR_BF16;
   const float sx = f16 ? kScaleX16 : 1.0f, sa = f16 ? kScaleA16 : 1.0f, sb = f16 ? kScaleB16 : 1.0f;
-  bool any_quintic = false, all_quintic = true;
-  for (int t = 0; t < p.iters; ++t) {
-    any_quintic |= p.coeffs[3 * t + 2] != 0.0;
-    all_quintic &= p.coeffs[3 * t + 2] != 0.0;
-  }
-  // Gram-space iteration (opt-in: its 16-bit state loses accuracy on
-  // ill-conditioned spectra), for matrices with Qp >= 2 Pp (see gram_space_scale)
-  double sm = 1.0;
-  const bool gs_ok = (p.flags & SLORR_GRAM_SPACE) && all_quintic && p.iters >= 2 &&
-                     gram_space_scale(p.coeffs.data(), p.iters, f16, &sm);
-  p.m_scale = sm;
+  bool any_quintic = false;
+  for (int t = 0; t < p.iters; ++t) any_quintic |= p.coeffs[3 * t + 2] != 0.0;
 
   // canonical shapes, groups
   p.mats.assign(p.n, MatDesc{});
   std::map<std::pair<int32_t, int32_t>, int> groups;
   p.paper_flops = p.mfma_flops = p.weight_bytes = 0;
-  p.gs_count = 0;
   for (int i = 0; i < p.n; ++i) {
     const int64_t r = p.shapes[i].rows, c = p.shapes[i].cols;
     if (r < 0 || c < 0) throw std::invalid_argument("negative matrix dimension");
@@ -136,8 +100,6 @@ void build_plan(Plan &p) {
     d.Qp = round_up(d.Q, kTile);
     if (r * c > kMaxElems || int64_t(d.Pp) * d.Qp > kMaxElems)
       throw std::domain_error("matrix has more than 2^31 - 1 elements");
-    d.gs = (gs_ok && d.Qp >= 2 * d.Pp) ? 1 : 0;
-    p.gs_count += d.gs;
     groups[{d.P, d.Q}]++;
     p.paper_flops += p.iters * (4.0 * P * P * Q + 2.0 * P * P * P);
     p.weight_bytes += double(r) * c * p.elem_bytes();
@@ -206,13 +168,12 @@ void build_plan(Plan &p) {
 
   // Symmetric-output products of the Gram and poly launches: upper-
   // triangle tiles only; the kernel also stores the transpose of off-diagonal
-  // tiles. `prods` lists the products of one launch as (matrix, op, k extent);
+  // tiles. `prods` lists the products of one launch as (matrix, k extent);
   // the 256-tile is used for every product of the launch when all of them
   // allow it and the launch has at least `min_big` such tiles (it halves the
   // operand traffic per flop of the 128-tile but gives 4x fewer blocks).
   struct Prod {
     int mat;
-    int32_t op;
     int32_t k;
   };
   auto sym_list = [&](const std::vector<Prod> &prods, int64_t min_big, TileRange *out) {
@@ -230,36 +191,30 @@ void build_plan(Plan &p) {
       const int nt = p.mats[q.mat].Pp / tsize(cfg);
       for (int tm = 0; tm < nt; ++tm)
         for (int tn = tm; tn < nt; ++tn) {
-          Tile t = make_tile(q.mat, tm, tn, 0);
-          t.op = q.op;
-          j.tiles.push_back(t);
+          j.tiles.push_back(make_tile(q.mat, tm, tn, 0));
         }
       jobs.push_back(std::move(j));
     }
     for (int c = 0; c < kNumCfg; ++c) out[c] = TileRange{};
     out[cfg] = emit(std::move(jobs));
   };
-  // A_0 = X_0 X_0^T: long k ranges (K = Qp), so the 256-tile pays as soon as
-  // the set has one upper-triangle 256-tile per CU. The P x P products
-  // (K = Pp, the shortest) take it only with two per CU.
+  // A = X X^T: long k ranges (K = Qp), so the 256-tile pays as soon as the set
+  // has one upper-triangle 256-tile per CU. The P x P products (K = Pp, the
+  // shortest) take it only with two per CU.
   {
-    std::vector<Prod> g0, g1, pl;
+    std::vector<Prod> g0, pl;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
-      g0.push_back({i, kOpXX, d.Qp});
-      g1.push_back(d.gs ? Prod{i, kOpBC, d.Pp} : Prod{i, kOpXX, d.Qp});
-      pl.push_back({i, kOpPoly, d.Pp});
+      g0.push_back({i, d.Qp});
+      pl.push_back({i, d.Pp});
     }
     sym_list(g0, kCus, p.gram);
-    if (p.gs_count && T > 1) sym_list(g1, kMinBigTiles, p.gram2);
-    else std::copy(p.gram, p.gram + kNumCfg, p.gram2);
     sym_list(pl, kMinBigTiles, p.pp);
   }
   // Split-K Gram. A set with few Gram tiles (small P) but long K = Qp would
   // leave most CUs idle: every tile's k range is cut into parts (multiples of
   // kTile) so that the launch has about kMinGramUnits blocks; each part writes
-  // an fp32 partial tile, and a reduce launch adds the parts in order. Used
-  // for X_0 X_0^T, and for every step when no matrix is in Gram space.
+  // an fp32 partial tile, and a reduce launch adds the parts in order.
   p.gsplit = TileRange{};
   p.gred = TileRange{};
   p.gram_parts = 0;
@@ -297,124 +252,58 @@ void build_plan(Plan &p) {
       p.gred.count = int32_t(reds.size());
     }
   }
-  // Update launches: the X-space updates B X (P x Q), in Gram space
-  // M = B M_prev (P x P), all full outputs, and C = B A (P x P, upper tiles,
-  // stored mirrored); the gradient product M X_0 (P x Q, full). The tiles of the product
-  // that writes the trace partials of a matrix (its last X-space update; in
-  // Gram space the last M = B M_prev, see Op::Update) own one slot each,
-  // contiguous per matrix. A matrix's products form one job, row band by row
-  // band (every product of a band reads the same rows of B). The 256-tile
-  // needs 256-aligned padded dims and is used when the launch has at least
-  // min_big of them.
+  // Update launches: X' = B X (P x Q, full output). The tiles of the last
+  // update own one trace slot each, contiguous per matrix (the same list
+  // serves every step). The tiles of one matrix form one job, dispatched
+  // column panel by column panel: the Pp / ts tiles that read one panel of X
+  // run together on one XCD, so the panel is fetched into its L2 once. The
+  // 256-tile needs 256-aligned padded dims and is used when the launch has at
+  // least two such tiles per CU; fp32 sets use the 128-tile (the fp32 256-tile
+  // update with the trace epilogue does not fit the register file).
   int32_t slot = 0;
-  struct Full {
-    int mat;
-    int32_t op;
-    int32_t n;            // output columns (Qp or Pp)
-    bool upper;           // symmetric output: upper tiles only
-  };
-  auto full_list = [&](const std::vector<Full> &prods, bool slots, int64_t min_big, TileRange *out) {
-    int64_t big = 0;
-    bool all_big = !prods.empty();
-    for (const Full &q : prods) {
-      const MatDesc &d = p.mats[q.mat];
-      const int64_t nb = d.Pp / kBigTile, mb = q.n / kBigTile;
-      all_big &= d.Pp % kBigTile == 0 && q.n % kBigTile == 0;
-      big += q.upper ? nb * (nb + 1) / 2 : nb * mb;
-    }
-    const int cfg = (all_big && big >= min_big) ? kCfg256 : kCfg128;
-    const int ts = tsize(cfg);
-    std::vector<Job> jobs;
-    for (size_t f = 0; f < prods.size();) {
-      size_t e = f;                                // products f .. e-1: one matrix
-      while (e < prods.size() && prods[e].mat == prods[f].mat) ++e;
-      MatDesc &d = p.mats[prods[f].mat];
-      Job j{prods[f].mat, double(d.Pp), {}};
-      if (slots) d.trace_begin = slot;
-      auto add = [&](size_t q, int tm, int tn) {
-        Tile t = make_tile(prods[q].mat, tm, tn, slots ? slot++ : 0);
-        t.op = prods[q].op;
-        j.tiles.push_back(t);
-      };
-      bool any_upper = false;
-      for (size_t q = f; q < e; ++q) any_upper |= prods[q].upper;
-      if (!any_upper) {
-        // column panel by column panel: the Pp / ts tiles that read one panel
-        // of the right operand are dispatched together on one XCD, so the
-        // panel is fetched into its L2 once
-        for (size_t q = f; q < e; ++q)
-          for (int tn = 0; tn < prods[q].n / ts; ++tn)
-            for (int tm = 0; tm < d.Pp / ts; ++tm) add(q, tm, tn);
-      } else {
-        for (int tm = 0; tm < d.Pp / ts; ++tm)
-          for (size_t q = f; q < e; ++q)
-            for (int tn = prods[q].upper ? tm : 0; tn < prods[q].n / ts; ++tn) add(q, tm, tn);
-      }
-      if (slots) d.trace_end = slot;
-      jobs.push_back(std::move(j));
-      f = e;
-    }
-    for (int c = 0; c < kNumCfg; ++c) out[c] = TileRange{};
-    out[cfg] = emit(std::move(jobs));
-  };
   {
-    std::vector<Full> xs, first, mix, ms, fs;
+    int64_t big = 0;
+    bool all_big = !order.empty() && f16;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
-      if (d.gs) {
-        first.push_back({i, kOpBA, d.Pp, true});
-        mix.push_back({i, kOpBM, d.Pp, false});
-        mix.push_back({i, kOpBA, d.Pp, true});
-        ms.push_back({i, kOpBM, d.Pp, false});
-        fs.push_back({i, kOpBX, d.Qp, false});
-      } else {
-        xs.push_back({i, kOpBX, d.Qp, false});
-        ms.push_back({i, kOpBX, d.Qp, false});
-        first.push_back({i, kOpBX, d.Qp, false});
-        mix.push_back({i, kOpBX, d.Qp, false});
-      }
+      all_big &= d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0;
+      big += int64_t(d.Pp / kBigTile) * (d.Qp / kBigTile);
     }
-    // P x P products (K = Pp) take the 256-tile from one per CU (measured on
-    // ViT-B/16: 648 tiles of 256 beat 2484 of 128), except in the first
-    // step's launch (C = B A only: 324 tiles of 256 lose to 1188 of 128)
-    // trace slots: on the X-space updates (their last one writes the
-    // partials) or, with Gram-space matrices, on the last step's launch
-    for (int c = 0; c < kNumCfg; ++c) p.pq[c] = p.plast[c] = TileRange{};
-    if (p.gs_count == 0) full_list(xs, true, kMinBigTiles, p.pq);
-    full_list(first, false, kMinBigTiles, p.pqc);
-    if (p.gs_count) full_list(ms, true, kCus, p.plast);
-    full_list(fs, false, kMinBigTiles, p.fin);
-    full_list(mix, false, kCus, p.pqm);
+    const int cfg = (all_big && big >= kMinBigTiles) ? kCfg256 : kCfg128;
+    const int ts = tsize(cfg);
+    std::vector<Job> jobs;
+    for (int i : order) {
+      MatDesc &d = p.mats[i];
+      Job j{i, double(d.Pp), {}};
+      d.trace_begin = slot;
+      for (int tn = 0; tn < d.Qp / ts; ++tn)
+        for (int tm = 0; tm < d.Pp / ts; ++tm) j.tiles.push_back(make_tile(i, tm, tn, slot++));
+      d.trace_end = slot;
+      jobs.push_back(std::move(j));
+    }
+    for (int c = 0; c < kNumCfg; ++c) p.pq[c] = TileRange{};
+    p.pq[cfg] = emit(std::move(jobs));
   }
   p.trace_slots = slot;
+  // canonical 64 x 64 tiles: the norm (one partial slot each, contiguous per
+  // matrix, summed in tile order), the normalisation and the gradient; element
+  // runs of the original layout for the decoupled update
   p.chunks.clear();
   p.prep.first = int32_t(p.tiles.size());
+  int32_t nslot = 0;
   for (int i = 0; i < p.n; ++i) {
     MatDesc &d = p.mats[i];
     if (d.empty) continue;
+    d.norm_begin = nslot;
     for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
-      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, 0));
+      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, nslot++));
+    d.norm_end = nslot;
     const int64_t total = int64_t(d.rows) * d.cols;
-    d.chunk_begin = int32_t(p.chunks.size());
     for (int64_t b = 0; b < total; b += kChunk)
       p.chunks.push_back({i, int32_t(b), int32_t(std::min<int64_t>(kChunk, total - b)), 0});
-    d.chunk_end = int32_t(p.chunks.size());
   }
   p.prep.count = int32_t(p.tiles.size()) - p.prep.first;
-  // gradient tiles of the X-space matrices (the Gram-space gradient is a
-  // product, on the tiles of X_T = M X_0)
-  if (p.gs_count == 0) {
-    p.gradx = p.prep;
-  } else {
-    p.gradx.first = int32_t(p.tiles.size());
-    for (int i = 0; i < p.n; ++i) {
-      const MatDesc &d = p.mats[i];
-      if (d.empty || d.gs) continue;
-      for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
-        for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, 0));
-    }
-    p.gradx.count = int32_t(p.tiles.size()) - p.gradx.first;
-  }
+  p.norm_slots = nslot;
 
   // workspace layout
   size_t off = 0;
@@ -430,7 +319,7 @@ void build_plan(Plan &p) {
   p.off_tiles = take(sizeof(Tile) * p.tiles.size());
   p.off_chunks = take(sizeof(Chunk) * p.chunks.size());
   p.off_scal = take(sizeof(Scalars) * p.n);
-  p.off_sumsq = take(sizeof(double) * p.chunks.size());
+  p.off_sumsq = take(sizeof(double) * size_t(p.norm_slots));
   p.off_trace = take(sizeof(double) * p.trace_slots);
   p.off_gpart = take(sizeof(float) * size_t(kTile) * kTile * size_t(p.gram_parts));
   p.off_static_end = off;
@@ -439,22 +328,12 @@ void build_plan(Plan &p) {
     MatDesc &d = p.mats[i];
     if (d.empty) continue;
     const size_t pq = size_t(d.Pp) * d.Qp * es, pp = size_t(d.Pp) * d.Pp * es;
-    d.x0 = take(pq);
-    d.x1 = d.gs ? d.x0 : take(pq);            // Gram space: X_0 only (X_T is never stored)
+    d.x[0] = take(pq);
+    d.x[1] = take(pq);
+    d.x[2] = take(pq);
     d.a = take(pp);
     d.b = any_quintic ? take(pp) : d.a;
-    if (d.gs) {
-      d.b1 = take(pp);
-      d.c = take(pp);
-      d.m0 = take(pp);
-      d.m1 = take(pp);
-      d.a0 = take(pp);
-      d.xt = d.x0;                            // unused: the gradient is a product
-    } else {
-      d.b1 = d.b;
-      d.c = d.m0 = d.m1 = d.a0 = d.a;
-      d.xt = (T & 1) ? d.x1 : d.x0;           // step t reads x[t & 1], writes the other
-    }
+    d.xt = d.x[xbuf(T)];                      // step t reads x[xbuf(t)], writes x[xbuf(t + 1)]
   }
   p.ws_bytes = off;
 
@@ -467,7 +346,7 @@ void build_plan(Plan &p) {
     l.tile_first = first;
     return l;
   };
-  if (!p.chunks.empty()) p.launches.push_back(plain(Op::SumSq, int32_t(p.chunks.size())));
+  if (p.prep.count) p.launches.push_back(plain(Op::SumSq, p.prep.count, p.prep.first));
   if (p.n > 0) p.launches.push_back(plain(Op::NormFin, (p.n + kThreads / 64 - 1) / (kThreads / 64)));
   if (p.prep.count) p.launches.push_back(plain(Op::Prep, p.prep.count, p.prep.first));
   auto gemm = [&](Op op, const TileRange *r, Launch l) {
@@ -480,20 +359,20 @@ void build_plan(Plan &p) {
       p.launches.push_back(l);
     }
   };
-  const float prod = float(1.0 / sb);           // (B_s Y_s) / s_b keeps Y's scale
+  const float prod = float(1.0 / sb);           // (B_s X_s) / s_b keeps X's scale
   for (int t = 0; t < T; ++t) {
     const double a = p.coeffs[3 * t], b = p.coeffs[3 * t + 1], c = p.coeffs[3 * t + 2];
-    const int32_t wx = t & 1;
+    const int32_t xi = xbuf(t), xo = xbuf(t + 1);
     const bool quintic = c != 0.0;
-    // A: A_s = s_a A with A = X X^T = (X_s X_s^T) / s_x^2; in Gram space
-    // (later steps) A = B C of the previous step
+    // the first step runs on X_0' = W / 2^e: its coefficients are scaled per
+    // matrix by kappa, kappa^3, kappa^5 (kappa = 2^e / (f + eps), read by the
+    // kernels), so that it computes p_1(X_0) with X_0 = kappa X_0'
+    const int32_t kap = t == 0 ? 1 : 0;
+    // A_s = s_a A with A = X X^T = (X_s X_s^T) / s_x^2
     Launch g{};
-    g.which_x = wx;
-    g.which_b = (t + 1) & 1;                  // B of the previous step
+    g.xin = xi;
     g.alpha = float(sa / (double(sx) * sx));
-    g.alpha2 = prod;
-    g.store_a0 = (t == 0 && p.gs_count) ? 1 : 0;
-    if (p.gsplit.count && (t == 0 || !p.gs_count)) {
+    if (p.gsplit.count) {
       g.op = Op::Gram;
       g.grid = p.gsplit.count;
       g.tile_first = p.gsplit.first;
@@ -501,55 +380,35 @@ void build_plan(Plan &p) {
       p.launches.push_back(g);                // fp32 partials
       Launch l = plain(Op::GramReduce, p.gred.count * kRedStripes, p.gred.first);
       l.alpha = g.alpha;
-      l.store_a0 = g.store_a0;
       p.launches.push_back(l);
     } else {
-      gemm(Op::Gram, t == 0 ? p.gram : p.gram2, g);
+      gemm(Op::Gram, p.gram, g);
     }
     const Op op = (t == T - 1) ? Op::Last : Op::Update;
     if (quintic) {
       // B_s = s_b (b A + c A A + a I) = s_b (b A_s / s_a + c (A_s A_s) / s_a^2 + a I):
-      // the step X' = a X + (b A + c A A) X becomes X' = B X. Gram-space
-      // matrices keep B_t in b[t & 1], so that B_0 serves as M_0.
+      // the step X' = a X + (b A + c A A) X becomes X' = B X (a_t I folded in)
       Launch l{};
-      l.which_x = wx;
-      l.which_b = t & 1;
+      l.xin = xi;
+      l.kap = kap;
       l.alpha = float(double(sb) * c / (double(sa) * sa));
       l.beta = float(double(sb) * b / sa);
       l.gamma = float(double(sb) * a);
       gemm(Op::Poly, p.pp, l);
-      // X'_s = (B_s X_s) / s_b; Gram space: M_t = B_t M_{t-1}, written to
-      // m[t & 1], read from m[(t - 1) & 1], or, at t = 1, M_0 = B_0 read from
-      // b: (B_s M_s) / s_b, or s_m (B_s B_0s) / s_b^2 at t = 1
+      // X'_s = (B_s X_s) / s_b
       Launch u{};
-      u.which_x = wx;
-      u.which_b = t & 1;
-      u.which_m = t & 1;
-      u.m_from_b = t == 1 ? 1 : 0;
+      u.xin = xi;
+      u.xout = xo;
       u.fold = 1;
       u.alpha = prod;
-      u.alpha2 = t == 1 ? float(sm / (double(sb) * sb)) : prod;
-      // and C = B A for the next step's A = B C (t < T - 1)
-      if (!p.gs_count) {
-        gemm(op, p.pq, u);
-      } else if (t == 0 && T > 1) {
-        gemm(Op::Update, p.pqc, u);
-      } else if (t < T - 1) {
-        gemm(Op::Update, p.pqm, u);
-      } else {
-        // one launch: the X-space last updates (trace against W) and the
-        // last M of the Gram-space matrices, whose trace partials follow from
-        // X_T = M X_0 and X_0 = W / (f + eps): sum(W * P) =
-        // (f + eps) tr(X_0^T M X_0) = (f + eps) tr(M A_0)
-        u.trace_m = 1;
-        u.tscale = float(1.0 / (sm * double(sa)));
-        gemm(Op::Last, p.plast, u);
-      }
+      gemm(op, p.pq, u);
     } else {
-      // cubic step (no Gram-space matrices): X'_s = a X_s + b (A_s X_s) / s_a
+      // cubic step: X'_s = a X_s + b (A_s X_s) / s_a
       Launch u{};
-      u.which_x = wx;
+      u.xin = xi;
+      u.xout = xo;
       u.use_a = 1;
+      u.kap = kap;
       u.alpha = float(b / sa);
       u.beta = float(a);
       gemm(op, p.pq, u);
@@ -557,26 +416,13 @@ void build_plan(Plan &p) {
   }
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
   p.launches.push_back(plain(Op::SetSum, 1));
-  // The gradient, once s1 and s2 are known: Gram space as the product
-  // s1 (M_{T-1} - r I) X_0 = s1 X_T - s2 W (r = s2 (f + eps) / s1, W =
-  // (f + eps) X_0) whose epilogue writes g times it (X_T is never stored),
-  // X space by the gradient kernel from the stored X_T. A deferred
-  // gradient runs the same launches later, from the M, X_0 and X_T the
-  // forward left in the workspace.
+  // The gradient, once s1 and s2 are known, by the gradient kernel from the
+  // stored X_T. A deferred gradient runs the same launch later, from the X_T
+  // and the factors the forward left in the workspace.
   p.grad_launches.clear();
   if (!(p.flags & SLORR_VALUES_ONLY)) {
     const size_t first = p.launches.size();
-    if (p.gs_count) {
-      Launch f{};
-      f.which_x = 0;
-      f.use_m = 1;
-      f.which_m = (T - 1) & 1;
-      f.fold = 1;
-      f.alpha = float(1.0 / sm);
-      f.mscale = float(sm);            // the scale of M: the shift r I is applied at it
-      gemm(Op::GradProd, p.fin, f);
-    }
-    if (p.gradx.count) p.launches.push_back(plain(Op::Grad, p.gradx.count, p.gradx.first));
+    if (p.prep.count) p.launches.push_back(plain(Op::Grad, p.prep.count, p.prep.first));
     p.grad_launches.assign(p.launches.begin() + first, p.launches.end());
     if (p.flags & SLORR_DEFER_GRAD) p.launches.resize(first);
   }
@@ -584,15 +430,14 @@ void build_plan(Plan &p) {
   // MFMA work the launches execute (padded, symmetric tiles counted once)
   p.mfma_flops = 0;
   for (const Launch &l : p.launches) {
-    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last && l.op != Op::GradProd)
-      continue;
+    if (l.op != Op::Gram && l.op != Op::Poly && l.op != Op::Update && l.op != Op::Last) continue;
     const double ts = tsize(l.cfg);
     for (int k = 0; k < l.grid; ++k) {
       const Tile &tl = p.tiles[l.tile_first + k];
       if (tl.mat < 0) continue;
       const MatDesc &d = p.mats[tl.mat];
       double kk = double(d.Pp);
-      if (l.op == Op::Gram && tl.op == kOpXX) kk = tl.k1 > 0 ? double(tl.k1 - tl.k0) : double(d.Qp);
+      if (l.op == Op::Gram) kk = tl.k1 > 0 ? double(tl.k1 - tl.k0) : double(d.Qp);
       p.mfma_flops += 2.0 * ts * ts * kk;
     }
   }

@@ -72,13 +72,12 @@ class Regularizer:
     """SLORR over a fixed list of weights (all of one dtype: float32 or bfloat16).
 
     kind "hoyer" (SLORR-Hoyer) or "nuclear" (SLORR-Nuc); iters, eps, ell,
-    degree, coeffs and gram_space as in Plan. Plans (and their workspaces) are
-    made on first use.
+    degree and coeffs as in Plan. Plans (and their workspaces) are made on
+    first use.
     """
 
     def __init__(self, params: Iterable[torch.Tensor], kind: str = "hoyer", iters: int = 6,
-                 eps: float = 0.0, ell: float = 1e-3, degree: int = 5, coeffs=None,
-                 gram_space: bool = False):
+                 eps: float = 0.0, ell: float = 1e-3, degree: int = 5, coeffs=None):
         self.params = list(params)
         if not self.params:
             raise ValueError("no parameters")
@@ -88,8 +87,7 @@ class Regularizer:
         self.dtype = _DT[next(iter(dts))]
         self.device = self.params[0].device
         self.shapes = [tuple(_as_matrix(p.detach()).shape) for p in self.params]
-        self.opts = dict(kind=kind, iters=iters, eps=eps, ell=ell, degree=degree, coeffs=coeffs,
-                         gram_space=gram_space)
+        self.opts = dict(kind=kind, iters=iters, eps=eps, ell=ell, degree=degree, coeffs=coeffs)
         self._plans = {}
 
     def plan(self, use: str) -> Plan:

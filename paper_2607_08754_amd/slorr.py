@@ -13,7 +13,7 @@ from typing import Optional, Sequence, Tuple
 import numpy as np
 
 from . import _lib
-from ._lib import ACCUMULATE, AUX, DEFER_GRAD, GRAM_SPACE, NO_GRAPH, VALUES_ONLY, SlorrError, check, lib
+from ._lib import ACCUMULATE, AUX, DEFER_GRAD, NO_GRAPH, VALUES_ONLY, SlorrError, check, lib
 
 __all__ = ["Plan", "pe_coefficients", "SlorrError", "HOYER", "NUCLEAR"]
 
@@ -45,24 +45,21 @@ class Plan:
     With defer_grad=True the call writes no gradient; plan.grad(weights,
     grads, scales) writes it afterwards from the state the call left.
     grad_dtype is the element type of the gradient buffers ("f32" / "bf16").
-    gram_space=True iterates the wide matrices (padded Q >= 2 P) in Gram
-    space: fewer flops, for well-conditioned weights only (its fp16 state
-    loses accuracy as sigma_min / sigma_max falls: past 2e-2 from ~0.1 on
-    some shapes).
     """
 
     def __init__(self, shapes: Sequence[Tuple[int, int]], dtype: str = "bf16", kind: str = HOYER,
                  iters: int = 6, degree: int = 5, ell: float = 1e-3, coeffs=None, eps: float = 0.0,
+                 safety: float = 0.01,
                  accumulate: bool = False, values_only: bool = False, graph: bool = True,
                  aux: bool = False, defer_grad: bool = False, grad_dtype: str = "f32",
-                 gram_space: bool = False, device=None, create_workspace: bool = True):
+                 device=None, create_workspace: bool = True):
         self.shapes = [(int(r), int(c)) for r, c in shapes]
         self.n = len(self.shapes)
         self.dtype, self.kind, self.iters = dtype, kind, int(iters)
         self.grad_dtype = grad_dtype
         self.flags = ((ACCUMULATE if accumulate else 0) | (VALUES_ONLY if values_only else 0)
                       | (0 if graph else NO_GRAPH) | (AUX if aux else 0)
-                      | (DEFER_GRAD if defer_grad else 0) | (GRAM_SPACE if gram_space else 0))
+                      | (DEFER_GRAD if defer_grad else 0))
         self.generation = 0          # forward calls enqueued so far
         self._c_shapes = _shapes_array(self.shapes)
         if grad_dtype not in _DTYPE:
@@ -71,6 +68,7 @@ class Plan:
         lib().slorr_default_options(ctypes.byref(opts))
         opts.iters, opts.degree, opts.ell, opts.eps, opts.flags = int(iters), int(degree), float(ell), float(eps), self.flags
         opts.grad_dtype = _DTYPE[grad_dtype]
+        opts.safety = float(safety) if safety > 0 else -1.0     # 0: no stabilisation
         self._coeffs = None
         if coeffs is not None:
             c = np.ascontiguousarray(np.asarray(coeffs, dtype=np.float64).reshape(-1))
@@ -82,8 +80,8 @@ class Plan:
         ws = ctypes.c_size_t()
         if dtype not in _DTYPE or kind not in _KIND:
             raise ValueError(f"dtype must be one of {list(_DTYPE)}, kind one of {list(_KIND)}")
-        check(lib().slorr_plan_create(ctypes.byref(self._handle), self.n, self._c_shapes, _DTYPE[dtype],
-                                      _KIND[kind], ctypes.byref(opts), ctypes.byref(ws)), "slorr_plan_create")
+        check(lib().slorr_plan(ctypes.byref(self._handle), self.n, self._c_shapes, _DTYPE[dtype],
+                               _KIND[kind], ctypes.byref(opts), ctypes.byref(ws)), "slorr_plan")
         self.workspace_bytes = int(ws.value)
         self.workspace = None
         self.device = None

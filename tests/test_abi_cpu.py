@@ -59,8 +59,8 @@ def _plan(L, shapes, dtype=0, kind=0, opts=None):
     h = ctypes.c_void_p()
     ws = ctypes.c_size_t()
     arr = (L.Shape * max(1, len(shapes)))(*[L.Shape(r, c) for r, c in shapes])
-    st = lib.slorr_plan_create(ctypes.byref(h), len(shapes), arr, dtype, kind,
-                               ctypes.byref(opts) if opts is not None else None, ctypes.byref(ws))
+    st = lib.slorr_plan(ctypes.byref(h), len(shapes), arr, dtype, kind,
+                        ctypes.byref(opts) if opts is not None else None, ctypes.byref(ws))
     return st, h, ws.value, arr
 
 
@@ -73,79 +73,54 @@ def _tri(P, t):
     return nt * (nt + 1) / 2 * float(t) * t
 
 
-def _expected_mfma(shapes, T, gram=False):
-    """MFMA work of the schedule. Symmetric products (A, B, C) run on upper-
-    triangle tiles: 256 x 256 when every matrix of the launch is 256-aligned
-    and the launch has one such tile per CU for X_0 X_0^T, two per CU for the
-    later A and the poly; full products (B X, M = B M_prev, X_T = M X_0) on all
-    tiles. C = B A runs in the update launch of its step (with the X-space
-    B X and, after the first step, M = B M_prev), whose tiles are 256 x 256
-    when all its products allow it and it has one per CU (two in the first
-    step). With gram=True (the opt-in flag) matrices with padded Q >= 2 P
-    iterate in Gram space."""
+def _expected_mfma(shapes, T):
+    """MFMA work of the schedule. Per step: A = X X^T on upper-triangle tiles
+    (256 x 256 when every matrix is 256-aligned and the launch has one such
+    tile per CU; else 128 x 128, split into k parts when there are fewer than
+    two tiles per CU: the parts cover each k once, so the work is the same),
+    the poly on upper-triangle tiles (256 x 256 from two per CU), B X on all
+    tiles (its work does not depend on the tile edge)."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
-    gs = [gram and Q >= 2 * P for P, Q in mats]
 
     def cfg(ps, min_big):
         big = sum((P // 256) * (P // 256 + 1) // 2 for P in ps)
         return 256 if ps and all(P % 256 == 0 for P in ps) and big >= min_big else 128
 
     ps = [P for P, _ in mats]
-    gps = [P for (P, _), g in zip(mats, gs) if g]
-    t0 = cfg(ps, 256)
-    tot = sum(2 * _tri(P, t0) * Q for P, Q in mats)                      # A = X_0 X_0^T
-    if gps and T > 1:
-        t1 = cfg(ps, 512)
-        tot += (T - 1) * sum(2 * _tri(P, t1) * (P if g else Q) for (P, Q), g in zip(mats, gs))
-        def ucfg(prods, min_big):              # (P, output columns, upper) of one update launch
-            big = sum((P // 256) * (P // 256 + 1) // 2 if up else (P // 256) * (N // 256) for P, N, up in prods)
-            ok = all(P % 256 == 0 and N % 256 == 0 for P, N, _ in prods)
-            return 256 if ok and big >= min_big else 128
-        sq = [(P, Q, False) for (P, Q), g in zip(mats, gs) if not g]
-        c = [(P, P, True) for P in gps]
-        tc0 = ucfg(sq + c, 512)
-        tcm = ucfg(sq + [(P, P, False) for P in gps] + c, 256)
-        tot += sum(2 * _tri(P, tc0) * P for P in gps)                   # C = B A, first step
-        tot += (T - 2) * sum(2 * _tri(P, tcm) * P for P in gps)         # C = B A, later steps
-        tot += (T - 1) * sum(2.0 * P ** 3 for P in gps)                  # M = B M_prev
-    else:
-        tot += (T - 1) * sum(2 * _tri(P, t0) * Q for P, Q in mats)
-    tp = cfg(ps, 512)
-    tot += T * sum(2 * _tri(P, tp) * P for P, _ in mats)                 # poly
-    tot += sum(2.0 * P * P * Q * (1 if g else T) for (P, Q), g in zip(mats, gs))   # B X, M X_0
-    return tot, sum(gs)
+    tg, tp = cfg(ps, 256), cfg(ps, 512)
+    return T * sum(2 * _tri(P, tg) * Q + 2 * _tri(P, tp) * P + 2.0 * P * P * Q for P, Q in mats)
 
 
-def _expected_mfma_x(shapes, T):
-    """MFMA work of an all-X-space schedule (no split-K): per step A = X X^T and
-    the poly on upper-triangle 128-tiles, B X on all tiles."""
+def _split_k(shapes):
+    """Whether the Gram launch is split into k parts (128-tiles, fewer than 512)."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
-    return T * sum(2 * _tri(P, 128) * Q + 2 * _tri(P, 128) * P + 2.0 * P * P * Q for P, Q in mats)
+    big = sum((P // 256) * (P // 256 + 1) // 2 for P, _ in mats)
+    if mats and all(P % 256 == 0 for P, _ in mats) and big >= 256:
+        return False
+    n128 = sum((P // 128) * (P // 128 + 1) // 2 for P, _ in mats)
+    return 0 < n128 < 512
 
 
-@pytest.mark.parametrize("gram", [False, True])
 @pytest.mark.parametrize("name", list(CONFIGS))
-def test_plan_facts(L, name, gram):
+def test_plan_facts(L, name):
     cfg = CONFIGS[name]
     lib = L.lib()
     opts = L.Options()
     lib.slorr_default_options(ctypes.byref(opts))
     opts.iters = cfg.iters
-    opts.flags = L.GRAM_SPACE if gram else 0
     st, h, ws, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER, opts)
     assert st == L.OK, lib.slorr_last_error()
     info = L.PlanInfo()
     assert lib.slorr_plan_get_info(h, ctypes.byref(info)) == L.OK
     assert info.n == cfg.n and info.iters == cfg.iters
     assert info.paper_flops == pytest.approx(cfg.flops(), rel=1e-12)
-    want, ngs = _expected_mfma(cfg.shapes, cfg.iters, gram)
-    assert info.gram_space == ngs
-    assert info.mfma_flops == pytest.approx(want, rel=1e-12)
+    assert info.mfma_flops == pytest.approx(_expected_mfma(cfg.shapes, cfg.iters), rel=1e-12)
     assert info.mfma_flops <= info.paper_flops * (1.0 if name in ("vit_b16", "vit_l16", "llm560") else 4.0)
     assert info.groups == len({(min(s), max(s)) for s in cfg.shapes})
-    # sumsq, norm, prep, the GEMM stages of each step (one or two tile classes
-    # each), X_T = M X_0, finalize, set sum, grad
-    assert 3 + 3 * cfg.iters + 3 <= info.launches <= 3 + 9 * cfg.iters + 5
+    # sumsq, norm, prep; per step the Gram (+ its reduce when split), the poly
+    # and the update; finalize, set sum, grad
+    per_step = 4 if _split_k(cfg.shapes) else 3
+    assert info.launches == 3 + per_step * cfg.iters + 3
     assert info.workspace_bytes == ws > 0
     esz = 2 if cfg.dtype == "bf16" else 4
     assert info.weight_bytes == sum(r * c * esz for r, c in cfg.shapes)
@@ -154,16 +129,13 @@ def test_plan_facts(L, name, gram):
 
 def test_plan_launch_work(L):
     """slorr_plan_get_launches: one kind per launch, algorithmic flops of the
-    products each performs. Over a call: X space (the default) T (2 P^2 Q
-    + 2 P^3 + 2 P^2 Q) (the paper's count); Gram space (opt-in, padded Q >= 2 P)
-    2 P^2 Q (X_0 X_0^T) + T 2 P^3 (poly) + 3 (T - 1) 2 P^3 (C = B A, A = B C,
-    M = B M) + 2 P^2 Q (X_T = M X_0)."""
+    products each performs; over a call T (2 P^2 Q + 2 P^3 + 2 P^2 Q), the
+    paper's count (Sec. 3 "Computational cost")."""
     lib = L.lib()
     opts = L.Options()
-    for name, gram in [(n, g) for n in ("tiny", "resnet18", "vit_b16", "llm560") for g in (False, True)]:
+    for name in ("tiny", "resnet18", "vit_b16", "llm560"):
         cfg = CONFIGS[name]
         lib.slorr_default_options(ctypes.byref(opts))
-        opts.flags = L.GRAM_SPACE if gram else 0
         st, h, _, _ = _plan(L, cfg.shapes, L.BF16 if cfg.dtype == "bf16" else L.F32, L.HOYER, opts)
         assert st == L.OK
         info = L.PlanInfo()
@@ -174,78 +146,17 @@ def test_plan_launch_work(L):
         te = (ctypes.c_int32 * nl)()
         assert lib.slorr_plan_get_launches(h, ops, fl, te) == L.OK
         names = [L.OPS[o] for o in ops]
-        gemm = ("gram", "poly", "update", "last", "grad_prod")
+        gemm = ("gram", "poly", "update", "last")
         assert all((e in (128, 256)) if o in gemm else e == 0 for o, e in zip(names, te))
-        ngs = sum(gram and _pad(max(s)) >= 2 * _pad(min(s)) for s in cfg.shapes)
-        tail = ["finalize", "setsum"] + ["grad_prod"] * (ngs > 0) + ["grad"] * (ngs < cfg.n)
-        assert names[:3] == ["sumsq", "norm", "prep"] and names[-len(tail):] == tail
+        assert names[:3] == ["sumsq", "norm", "prep"] and names[-3:] == ["finalize", "setsum", "grad"]
         T = info.iters                                     # the default options: T = 6
-        want = 0.0
-        for m, n in cfg.shapes:
-            P, Q = float(min(m, n)), float(max(m, n))
-            if gram and _pad(int(Q)) >= 2 * _pad(int(P)):
-                want += 4 * P * P * Q + 2 * P ** 3 * (T + 3 * (T - 1))
-            else:
-                want += T * (4 * P * P * Q + 2 * P ** 3)
+        assert names.count("last") == 1 and names.count("update") == T - 1 and names.count("poly") == T
+        want = sum(T * (4.0 * min(s) ** 2 * max(s) + 2.0 * min(s) ** 3) for s in cfg.shapes)
         assert sum(fl) == pytest.approx(want, rel=1e-12)
         assert all(f == 0.0 for f, o in zip(fl, names) if o not in gemm)
         assert lib.slorr_plan_get_launches(h, None, None, None) == L.OK
         lib.slorr_plan_destroy(h)
     assert lib.slorr_plan_get_launches(None, None, None, None) == L.ERR_INVALID_ARGUMENT
-
-
-def test_plan_gram_space_selection(L):
-    """Gram space is opt-in (GRAM_SPACE) and then taken for padded Q >= 2 P and
-    quintic tables only; without the flag, with a cubic table, or with a table
-    whose M would not fit the fp16 iterate, every matrix stays in X space."""
-    shapes = [(128, 256), (256, 128), (128, 255), (384, 640), (256, 256), (64, 576)]
-    opts = L.Options()
-    L.lib().slorr_default_options(ctypes.byref(opts))
-    opts.flags = L.GRAM_SPACE
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
-    assert st == L.OK
-    info = L.PlanInfo()
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 4          # 128 x 256 both ways, 128 x 255, 64 x 576 (padded 128 x 640)
-    # fp16 iterate: M's scale is a power of two with |M| s_m <= 2^14
-    assert info.m_scale > 0 and math.log2(info.m_scale) == int(math.log2(info.m_scale))
-    L.lib().slorr_plan_destroy(h)
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)         # the default: the paper's form
-    assert st == L.OK
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 0
-    L.lib().slorr_plan_destroy(h)
-    opts.flags = 0                                         # options without the flag
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
-    assert st == L.OK
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 0
-    assert info.mfma_flops == pytest.approx(_expected_mfma_x(shapes, info.iters), rel=1e-12)
-    L.lib().slorr_plan_destroy(h)
-    L.lib().slorr_default_options(ctypes.byref(opts))
-    opts.flags = L.GRAM_SPACE
-    opts.degree = 3
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
-    assert st == L.OK
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 0
-    L.lib().slorr_plan_destroy(h)
-    # a table whose products grow beyond the fp16 range: a = 2^10 each step
-    tab = (ctypes.c_double * 9)(*([1024.0, 0.0, 1e-9] * 3))
-    L.lib().slorr_default_options(ctypes.byref(opts))
-    opts.flags = L.GRAM_SPACE
-    opts.iters = 3
-    opts.coeffs = ctypes.cast(tab, ctypes.POINTER(ctypes.c_double))
-    st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
-    assert st == L.OK
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 0
-    L.lib().slorr_plan_destroy(h)
-    # fp32: no range limit on M
-    st, h, _, _ = _plan(L, shapes, L.F32, L.HOYER, opts)
-    L.lib().slorr_plan_get_info(h, ctypes.byref(info))
-    assert info.gram_space == 4 and info.m_scale == 1.0
-    L.lib().slorr_plan_destroy(h)
 
 
 def test_empty_plans(L):
@@ -260,17 +171,17 @@ def test_empty_plans(L):
     L.lib().slorr_plan_destroy(h)
 
 
-def test_plan_create_errors(L):
+def test_plan_errors(L):
     lib = L.lib()
     h = ctypes.c_void_p(1234)
     ws = ctypes.c_size_t()
     one = (L.Shape * 1)(L.Shape(4, 8))
     # null out-pointers / shapes, negative n
-    assert lib.slorr_plan_create(None, 1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
-    assert lib.slorr_plan_create(ctypes.byref(h), 1, one, 0, 0, None, None) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan(None, 1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan(ctypes.byref(h), 1, one, 0, 0, None, None) == L.ERR_INVALID_ARGUMENT
     assert h.value is None                                    # set to NULL on error
-    assert lib.slorr_plan_create(ctypes.byref(h), 1, None, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
-    assert lib.slorr_plan_create(ctypes.byref(h), -1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan(ctypes.byref(h), 1, None, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
+    assert lib.slorr_plan(ctypes.byref(h), -1, one, 0, 0, None, ctypes.byref(ws)) == L.ERR_INVALID_ARGUMENT
     assert b"n must be" in lib.slorr_last_error()
     # bad shapes
     for r, c, want in [(-1, 4, L.ERR_INVALID_ARGUMENT), (16385, 16385, L.ERR_UNSUPPORTED),
@@ -295,6 +206,7 @@ def test_plan_create_errors(L):
     assert with_opts(eps=-1.0) == L.ERR_INVALID_ARGUMENT
     assert with_opts(eps=float("inf")) == L.ERR_INVALID_ARGUMENT
     assert with_opts(flags=0x100) == L.ERR_INVALID_ARGUMENT
+    assert with_opts(flags=0x20) == L.ERR_INVALID_ARGUMENT      # no such flag
     bad = (ctypes.c_double * 18)(*([1.0] * 17 + [float("nan")]))
     assert with_opts(coeffs=ctypes.cast(bad, ctypes.POINTER(ctypes.c_double))) == L.ERR_INVALID_ARGUMENT
     assert with_opts() == L.OK
@@ -320,7 +232,6 @@ def test_call_errors_before_any_device_use(L):
     w = (ctypes.c_void_p * 2)(0x20000, 0x30000)
     g = (ctypes.c_void_p * 2)(0x40000, 0x50000)
     call = lib.slorr_reg_fwd_bwd
-    assert call(None, 2, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
     assert call(h, 3, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
     assert call(h, 2, w, shapes, 1, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
     assert call(h, 2, w, shapes, 0, 5, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
@@ -434,37 +345,54 @@ def test_deferred_gradient_and_apply_checks_before_device_use(L):
 
 
 def test_split_k_gram_plan(L):
-    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch:
-    every step for X-space matrices, the first step (X_0 X_0^T) for Gram-space
-    ones; the parts cover every k exactly once (same executed MFMA work as one
-    pass per tile). Sets with enough tiles are not split."""
+    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch
+    in every step; the parts cover every k exactly once (same executed MFMA
+    work as one pass per tile). Sets with enough tiles are not split."""
     def facts(shapes):
-        opts = L.Options()
-        L.lib().slorr_default_options(ctypes.byref(opts))
-        opts.flags = L.GRAM_SPACE
-        st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER, opts)
+        st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
         assert st == L.OK
         info = L.PlanInfo()
         L.lib().slorr_plan_get_info(h, ctypes.byref(info))
         L.lib().slorr_plan_destroy(h)
         return info
     T = 6
-    xs = [(384, 640), (640, 384), (256, 384)]                # X space: padded Q < 2 P
-    info = facts(xs)
-    assert info.gram_space == 0
-    assert info.launches == 3 + 4 * T + 3                    # gram parts, reduce, poly, update
-    assert info.mfma_flops == pytest.approx(_expected_mfma(xs, T, True)[0], rel=1e-12)
-    gs = [(256, 4096), (4096, 256), (384, 2944)]             # Gram space, 3 + 3 + 6 Gram tiles
-    info = facts(gs)
-    assert info.gram_space == 3
-    # first step: gram parts, reduce, poly, C = B A; later steps: A = B C, poly,
-    # one update launch with M = B M_prev and C = B A (no C in the last step);
-    # finalize, set sum, then the gradient as the product X_T = M X_0 (no
-    # gradient kernel: no X-space matrix)
-    assert info.launches == 3 + 4 + 3 * (T - 2) + 3 + 3
-    assert info.mfma_flops == pytest.approx(_expected_mfma(gs, T, True)[0], rel=1e-12)
-    # no split: per step A, poly, one update launch (B X, B M, B A; the last
-    # step's with the trace partials of both kinds); finalize, set sum, the
-    # Gram-space gradient product, the X-space gradient
+    for shapes in ([(384, 640), (640, 384), (256, 384)], [(256, 4096), (4096, 256), (384, 2944)]):
+        assert _split_k(shapes)
+        info = facts(shapes)
+        assert info.launches == 3 + 4 * T + 3                # gram parts, reduce, poly, update
+        assert info.mfma_flops == pytest.approx(_expected_mfma(shapes, T), rel=1e-12)
     big = facts(CONFIGS["vit_b16"].shapes)
-    assert big.launches == 3 + 3 * 6 + 4
+    assert not _split_k(CONFIGS["vit_b16"].shapes)
+    assert big.launches == 3 + 3 * T + 3
+
+
+def test_null_plan_checks_before_device_use(L):
+    """slorr_reg_fwd_bwd with plan == NULL (the internal plan cache) rejects
+    bad arguments before it selects a device or builds a plan; and the cache
+    configuration and release entry points need no device."""
+    lib = L.lib()
+    one = (L.Shape * 1)(L.Shape(4, 8))
+    w = (ctypes.c_void_p * 1)(0x20000)
+    g = (ctypes.c_void_p * 1)(0x40000)
+    vals = ctypes.c_void_p(0x10000)
+    call = lib.slorr_reg_fwd_bwd
+    lib.slorr_cache_config(L.F32, None)
+    assert call(None, -1, w, one, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, w, None, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, None, one, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, w, one, 0, 0, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, w, one, 0, 6, None, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, w, one, 0, 6, ctypes.c_void_p(0x10002), g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(None, 1, w, one, 0, 6, vals, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert b"out_grads" in lib.slorr_last_error()
+    o = L.Options()
+    lib.slorr_default_options(ctypes.byref(o))
+    o.flags = L.VALUES_ONLY
+    tab = (ctypes.c_double * 9)(*([1.875, -1.25, 0.375] * 3))
+    o.iters = 3
+    o.coeffs = ctypes.cast(tab, ctypes.POINTER(ctypes.c_double))
+    lib.slorr_cache_config(L.BF16, ctypes.byref(o))          # copies the table
+    del tab
+    assert call(None, 1, w, one, 0, 6, None, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    lib.slorr_cache_config(L.F32, None)
+    assert lib.slorr_cache_clear() == L.OK                   # empty cache: no device call

@@ -35,11 +35,7 @@ def test_bench_alg_bytes_vit_b16():
     cfg = CONFIGS["vit_b16"]
     pq = sum(m * n for m, n in cfg.shapes)
     assert pq == 84934656
-    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "sumsq", False) == 2 * pq
-    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "prep", False) == 4 * pq
-    # X space: W and X_T read, fp32 gradient written, every matrix
-    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "grad", False) == 8 * pq
-    # opt-in Gram space: only the 12 square matrices keep the gradient kernel
-    sq = sum(m * n for m, n in cfg.shapes if m == n)
-    assert sq == 12 * 768 * 768
-    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "grad", True) == 8 * sq
+    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "sumsq") == 2 * pq
+    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "prep") == 4 * pq
+    # W and X_T read, fp32 gradient written, every matrix
+    assert bench._alg_bytes_per_launch(cfg.shapes, "bf16", "grad") == 8 * pq

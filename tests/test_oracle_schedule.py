@@ -11,7 +11,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle.pe_schedule import E_STOP, apply_scalar, greedy_step, pe_schedule
+from oracle.pe_schedule import E_STOP, apply_scalar, default_table, greedy_step, pe_schedule, stabilize
 
 GOLDEN = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.json")))
 
@@ -125,3 +125,37 @@ def test_scalar_map_is_odd_and_zero_at_zero():
     assert apply_scalar(tab, np.array([0.0]))[0] == 0.0
     # slope at 0 is prod a_t (the small-singular-value gain)
     assert apply_scalar(tab, np.array([1e-12]))[0] / 1e-12 == pytest.approx(np.prod(tab[:, 0]), rel=1e-9)
+
+
+def _perturbed_map(tab, x, push):
+    """The scalar map with every intermediate value pushed up by the factor
+    (1 + push) before each step: the worst direction of an iterate's rounding
+    near the top of an interval."""
+    y = np.asarray(x, dtype=np.float64).copy()
+    for a, b, c in tab:
+        y = y * (1.0 + push)
+        y = a * y + b * y ** 3 + c * y ** 5
+    return y
+
+
+def test_stabilised_table():
+    """default_table = the greedy rows with every step but the last evaluated
+    at x / (1 + delta): the rows are the argument-scaled polynomials (checked
+    as values of p_t at sample points), delta = 0 leaves the table unchanged,
+    and the property the scaling is for holds: with every intermediate value
+    pushed up by 0.5 % (a rounding-sized perturbation at the steep top end of
+    an interval) the stabilised map stays within 2 % of 1 on [l, 1], while the
+    plain greedy map leaves the polynomials' controlled range."""
+    raw = pe_schedule(6)
+    assert np.array_equal(stabilize(raw, 0.0), raw)
+    tab = default_table(6)
+    assert np.array_equal(tab[-1], raw[-1])
+    xs = np.linspace(-1.5, 1.5, 301)
+    for t in range(5):
+        want = _poly(raw[t], xs / 1.01)
+        assert np.allclose(_poly(tab[t], xs), want, rtol=1e-13, atol=1e-13)
+    x = np.linspace(1e-3, 1.0, 100001)
+    assert np.max(np.abs(1.0 - _perturbed_map(tab, x, 0.005))) <= 0.02
+    assert np.max(np.abs(_perturbed_map(raw, x, 0.005))) > 10.0
+    # the unperturbed stabilised map still converges on [l, 1]
+    assert np.max(np.abs(1.0 - apply_scalar(tab, x))) <= 4e-3
