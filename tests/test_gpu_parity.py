@@ -164,14 +164,16 @@ def test_rank_deficient(dtype, rank):
     down to 0.025, rounded to the storage type) on wide, tall and square
     matrices. The approximation guarantee covers singular values in [ell, 1]
     after normalisation (App. C, the remark on zero singular values); in the
-    other directions any finite-precision iterate adds rounding noise that the
+    null directions any finite-precision iterate adds rounding noise that the
     polynomials scale up (p_s(x) ~ a_s x for x << ell). Checked against the
-    oracle: the value, and the gradient off the block on the two null spaces,
-    at the usual tolerance (rank 1 Hoyer is a stationary point: relative to
-    s1 P); the null-space block at the error model's bound
-    gain * (u_iter + sqrt(K) u_acc) * ||s1 P_ref||_F, gain = sum_t prod_{s>t} a_s
-    (the noise added after step t, scaled by the later steps), u_iter the
-    iterate's unit roundoff, u_acc that of the fp32 accumulation over K terms."""
+    oracle: the value, and the gradient's block on the range (U_r U_r^T D V_r V_r^T,
+    D the difference) at the usual tolerance (rank 1 Hoyer is a stationary
+    point: relative to s1 P); the rest of D (the blocks that touch a null space)
+    against the error model's size gain * (u_iter + sqrt(K) u_acc) * ||s1 P_ref||_F,
+    gain = sum_t prod_{s>t} a_s (the noise added after step t, scaled by the
+    later steps), u_iter the iterate's unit roundoff, sqrt(K) u_acc the typical
+    error of an fp32 sum of K terms; the model gives the size, not a bound, so
+    the test allows 3 times it."""
     g, eps = 0.6, 1e-4
     tol = TOL[dtype]
     gain = noise_gain(default_table(6))
@@ -186,25 +188,25 @@ def test_rank_deficient(dtype, rank):
         refs = run_oracle(arrs, dtype, kind, 6, eps=eps, g=g)
         for i, (a, G, ref) in enumerate(zip(arrs, grads, refs)):
             U, _, Vt = np.linalg.svd(widen(a, dtype).astype(np.float64), full_matrices=False)
-            Nu = np.eye(a.shape[0]) - U[:, :rank] @ U[:, :rank].T
-            Nv = np.eye(a.shape[1]) - Vt[:rank].T @ Vt[:rank]
+            Ru = U[:, :rank] @ U[:, :rank].T
+            Rv = Vt[:rank].T @ Vt[:rank]
             D = G - ref.grad
-            null = Nu @ D @ Nv
-            off = D - null
+            rng = Ru @ D @ Rv
+            rest = D - rng
             s1p = first_term(ref, kind, g)
             scale = s1p if stationary else ref.grad
             ve = value_err(vals[i], ref)
-            ge = np.linalg.norm(off) / np.linalg.norm(scale)
-            gm = np.abs(off).max() / np.abs(scale).max()
+            ge = np.linalg.norm(rng) / np.linalg.norm(scale)
+            gm = np.abs(rng).max() / np.abs(scale).max()
             K = max((s + 127) // 128 * 128 for s in a.shape)
-            bound = gain * (U_ITER[dtype] + np.sqrt(K) * U_ACC) * np.linalg.norm(s1p)
-            print(f"[parity] rank {rank} {dtype} {kind} {a.shape}: value err {ve:.2e}, off the null block: "
-                  f"grad err {ge:.2e} element-wise {gm:.2e}; null block err / bound "
-                  f"{np.linalg.norm(null) / bound:.3f} (bound {bound / np.linalg.norm(s1p):.2e} ||s1 P||)",
+            bound = 3.0 * gain * (U_ITER[dtype] + np.sqrt(K) * U_ACC) * np.linalg.norm(s1p)
+            print(f"[parity] rank {rank} {dtype} {kind} {a.shape}: value err {ve:.2e}, range block: "
+                  f"grad err {ge:.2e} element-wise {gm:.2e}; the rest / bound "
+                  f"{np.linalg.norm(rest) / bound:.3f} (bound {bound / np.linalg.norm(s1p):.2e} ||s1 P||)",
                   flush=True)
             assert np.isfinite(vals[i]) and ve <= tol, (i, ve)
             assert ge <= tol and gm <= tol, (i, ge, gm)
-            assert np.linalg.norm(null) <= bound, (i, np.linalg.norm(null), bound)
+            assert np.linalg.norm(rest) <= bound, (i, np.linalg.norm(rest), bound)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
