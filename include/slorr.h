@@ -270,6 +270,27 @@ SLORR_API slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n
                                  void *const *out_grads, float grad_scale, void *stream,
                                  float *launch_ms, int32_t *launch_op);
 
+/* For callers that cannot allocate device memory (tight serving loops, code
+ * running where hipMalloc is not allowed): slorr_reg_fwd_bwd with the same
+ * arguments, results and rounding, run in a static scratch array the library
+ * holds on each GPU (64 MiB, SLORR_SCRATCH_BYTES; each GPU the library runs on
+ * keeps it until the process ends) instead of the plan's workspace. The plan
+ * needs no workspace attached; its workspace size (slorr_plan's
+ * workspace_bytes) must be at most SLORR_SCRATCH_BYTES, else
+ * SLORR_ERR_WORKSPACE. The call allocates nothing: it copies the plan's tables
+ * into the array (ordered on `stream`) and enqueues the schedule launch by
+ * launch (no graph). Every call on one GPU shares that GPU's array, which keeps
+ * the last call's contents (no part of it has to start at zero): calls that
+ * overlap on one GPU, on different streams or from different threads, race;
+ * order them on one stream. The iterate state stays in the array, so a plan
+ * with SLORR_DEFER_GRAD is refused (SLORR_ERR_INVALID_ARGUMENT) and no
+ * slorr_reg_grad may follow. */
+#define SLORR_SCRATCH_BYTES ((size_t)64 << 20)
+SLORR_API slorr_status_t slorr_reg_fwd_bwd_noalloc(slorr_plan_t plan, int32_t n, const void *const *weights,
+                                 const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                                 float *out_vals, void *const *out_grads, float grad_scale,
+                                 void *stream);
+
 /* Release the plan (and its captured graph). Does not free the workspace.
  * Synchronises with work the plan has enqueued. NULL is accepted. */
 SLORR_API slorr_status_t slorr_plan_destroy(slorr_plan_t plan);

@@ -36,7 +36,7 @@ OPS = ("sumsq", "norm", "prep", "gram", "poly", "update", "last", "finalize", "g
 EXPORTED = ("slorr_default_options", "slorr_pe_coefficients", "slorr_plan", "slorr_cache_config",
             "slorr_cache_clear",
             "slorr_plan_set_workspace", "slorr_reg_fwd_bwd", "slorr_reg_grad", "slorr_decoupled_apply",
-            "slorr_reg_fwd_bwd_profiled",
+            "slorr_reg_fwd_bwd_profiled", "slorr_reg_fwd_bwd_noalloc",
             "slorr_plan_destroy", "slorr_plan_get_info", "slorr_plan_get_launches", "slorr_status_string",
             "slorr_last_error")
 
@@ -106,6 +106,9 @@ def lib() -> ctypes.CDLL:
                                                  ctypes.c_int, i32, vp, ctypes.POINTER(vp), ctypes.c_float, vp,
                                                  ctypes.POINTER(ctypes.c_float), ctypes.POINTER(i32)]
         L.slorr_reg_fwd_bwd_profiled.restype = ctypes.c_int
+        L.slorr_reg_fwd_bwd_noalloc.argtypes = [vp, i32, ctypes.POINTER(vp), ctypes.POINTER(Shape), ctypes.c_int,
+                                                i32, vp, ctypes.POINTER(vp), ctypes.c_float, vp]
+        L.slorr_reg_fwd_bwd_noalloc.restype = ctypes.c_int
         L.slorr_plan_destroy.argtypes = [vp]
         L.slorr_plan_destroy.restype = ctypes.c_int
         L.slorr_plan_get_info.argtypes = [vp, ctypes.POINTER(PlanInfo)]

@@ -110,11 +110,12 @@ slorr::Plan &check_call(slorr_plan_t plan, int32_t n, const void *const *weights
 
 // Pointer checks of weights and (if want_grad) gradient buffers, and that no
 // gradient range overlaps a weight range or another gradient range.
-void check_buffers(const slorr::Plan &p, const void *const *weights, void *const *out_grads,
+void check_buffers(slorr::Plan &p, const void *const *weights, void *const *out_grads,
                    bool want_grad) {
   const int n = p.n;
   if (want_grad && n > 0 && !out_grads) throw std::invalid_argument("out_grads is NULL");
-  std::vector<std::pair<uintptr_t, std::pair<uintptr_t, int>>> spans;  // begin, (end, is_grad)
+  auto &spans = p.spans;              // begin, (end, is_grad); capacity 2 n from the plan
+  spans.clear();
   for (int i = 0; i < n; ++i) {
     const slorr::MatDesc &d = p.mats[i];
     if (d.empty) continue;
@@ -626,6 +627,46 @@ slorr_status_t slorr_reg_fwd_bwd_profiled(slorr_plan_t plan, int32_t n,
       launch_ms[i] = ms;
       if (launch_op) launch_op[i] = int32_t(p.launches[i].op);
     }
+    return SLORR_OK;
+  });
+}
+
+slorr_status_t slorr_reg_fwd_bwd_noalloc(slorr_plan_t plan, int32_t n, const void *const *weights,
+                                         const slorr_shape_t *shapes, slorr_kind_t kind, int32_t iters,
+                                         float *out_vals, void *const *out_grads, float grad_scale,
+                                         void *stream) {
+  return guarded([&]() -> slorr_status_t {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    slorr::Plan &p = check_call(plan, n, weights, shapes, bits(kind), iters);
+    if (p.flags & SLORR_DEFER_GRAD)
+      throw std::invalid_argument("SLORR_DEFER_GRAD needs the plan's own workspace (slorr_reg_fwd_bwd)");
+    if (!out_vals) throw std::invalid_argument("out_vals is NULL");
+    if (!aligned(out_vals, 4)) throw std::invalid_argument("out_vals must be 4-byte aligned");
+    const bool want_grad = !(p.flags & SLORR_VALUES_ONLY);
+    check_buffers(p, weights, out_grads, want_grad);
+    if (p.ws_bytes > slorr::kScratchBytes)
+      throw ApiError{SLORR_ERR_WORKSPACE, "the plan needs " + std::to_string(p.ws_bytes) +
+                                              " bytes of workspace; the static scratch holds " +
+                                              std::to_string(slorr::kScratchBytes)};
+    void *scr = slorr::scratch_address();
+    // the call's pointer table into the host image, then the whole table
+    // region to the scratch array, ordered on the caller's stream
+    char *img = p.image.data();
+    auto *dyn = reinterpret_cast<slorr::DynDesc *>(img + p.off_dyn);
+    for (int i = 0; i < n; ++i) {
+      dyn[i].w = p.mats[i].empty ? nullptr : weights[i];
+      dyn[i].g = (want_grad && !p.mats[i].empty) ? out_grads[i] : nullptr;
+    }
+    slorr::CallParams call{};
+    call.out_vals = out_vals;
+    call.gscale = nullptr;
+    call.grad_scale = grad_scale;
+    std::memcpy(img + p.off_call, &call, sizeof(call));
+    hip_check(hipMemcpyAsync(scr, img, p.image.size(), hipMemcpyHostToDevice, s), "hipMemcpyAsync tables");
+    // the iterate state of this call lives in the scratch array, not in the
+    // plan's workspace: no deferred gradient can follow it
+    p.state_ready = false;
+    slorr::enqueue(p, s, nullptr, scr);
     return SLORR_OK;
   });
 }

@@ -29,6 +29,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <type_traits>
@@ -554,8 +555,7 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPai
 }
 
 template <typename Tw, typename Tx>
-void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev) {
-  const char *ws = static_cast<const char *>(p.ws);
+void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev, const char *ws) {
   const Tile *tiles = reinterpret_cast<const Tile *>(ws + p.off_tiles) + l.tile_first;
   const MatDesc *mats = reinterpret_cast<const MatDesc *>(ws + p.off_mats);
   const DynDesc *dyn = reinterpret_cast<const DynDesc *>(ws + p.off_dyn);
@@ -570,8 +570,7 @@ void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev
 }
 
 template <typename Tw, typename Tx>
-void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev) {
-  char *ws = static_cast<char *>(p.ws);
+void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev, char *ws) {
   const MatDesc *mats = reinterpret_cast<const MatDesc *>(ws + p.off_mats);
   const DynDesc *dyn = reinterpret_cast<const DynDesc *>(ws + p.off_dyn);
   const CallParams *call = reinterpret_cast<const CallParams *>(ws + p.off_call);
@@ -634,7 +633,7 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev)
         go(k_setsum, dim3(1), dim3(1024), s, ev, sc, call, p.n);
         break;
       case Op::Grad:
-        launch_grad<Tw, Tx>(p, l, s, ev);
+        launch_grad<Tw, Tx>(p, l, s, ev, ws);
         break;
     }
     check(hipGetLastError(), "kernel launch");
@@ -643,13 +642,14 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev)
 
 }  // namespace
 
-void enqueue(const Plan &p, hipStream_t s, hipEvent_t *events) {
+void enqueue(const Plan &p, hipStream_t s, hipEvent_t *events, void *ws) {
+  char *w = static_cast<char *>(ws ? ws : p.ws);
   for (size_t li = 0; li < p.launches.size(); ++li) {
     const EvPair pair{events ? events[2 * li] : nullptr, events ? events[2 * li + 1] : nullptr};
     if (p.dtype == SLORR_BF16)
-      launch_one<bf16_t, _Float16>(p, p.launches[li], s, events ? &pair : nullptr);
+      launch_one<bf16_t, _Float16>(p, p.launches[li], s, events ? &pair : nullptr, w);
     else
-      launch_one<float, float>(p, p.launches[li], s, events ? &pair : nullptr);
+      launch_one<float, float>(p, p.launches[li], s, events ? &pair : nullptr, w);
   }
 }
 
@@ -672,12 +672,38 @@ void enqueue_apply(const Plan &p, hipStream_t s) {
 }
 
 void enqueue_grad(const Plan &p, hipStream_t s) {
+  char *w = static_cast<char *>(p.ws);
   for (const Launch &l : p.grad_launches) {
     if (p.dtype == SLORR_BF16)
-      launch_one<bf16_t, _Float16>(p, l, s, nullptr);
+      launch_one<bf16_t, _Float16>(p, l, s, nullptr, w);
     else
-      launch_one<float, float>(p, l, s, nullptr);
+      launch_one<float, float>(p, l, s, nullptr, w);
   }
+}
+
+// ------------------------------------------------------ static scratch
+// The workspace of the entry point that allocates nothing: one array per GPU
+// in the library's code object (each GPU the library runs on holds it until
+// the process ends). In host code `scratch` names a host-side stand-in, not
+// the device array: its device address is taken once per device with
+// hipGetSymbolAddress and used from then on.
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+void *scratch_address() {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *ptr[kMaxDevices] = {};
+  int dev = -1;
+  check(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) throw HipError("device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void *a = nullptr;
+    check(hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!a) throw HipError("hipGetSymbolAddress(scratch) returned NULL");
+    ptr[dev] = a;
+  }
+  return ptr[dev];
 }
 
 }  // namespace slorr

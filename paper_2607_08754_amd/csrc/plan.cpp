@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstring>
 #include <map>
 #include <stdexcept>
 #include <utility>
@@ -336,6 +337,13 @@ void build_plan(Plan &p) {
     d.xt = d.x[xbuf(T)];                      // step t reads x[xbuf(t)], writes x[xbuf(t + 1)]
   }
   p.ws_bytes = off;
+  // host image of the table region, for the entry point that allocates nothing
+  p.image.assign(p.off_scal, 0);
+  if (p.n) std::memcpy(p.image.data() + p.off_mats, p.mats.data(), sizeof(MatDesc) * p.n);
+  if (!p.tiles.empty()) std::memcpy(p.image.data() + p.off_tiles, p.tiles.data(), sizeof(Tile) * p.tiles.size());
+  if (!p.chunks.empty()) std::memcpy(p.image.data() + p.off_chunks, p.chunks.data(), sizeof(Chunk) * p.chunks.size());
+  p.spans.clear();
+  p.spans.reserve(size_t(2) * p.n);
 
   // launch schedule
   p.launches.clear();

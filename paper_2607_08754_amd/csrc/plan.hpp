@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "layout.hpp"
@@ -97,6 +98,11 @@ struct Plan {
   bool state_ready = false;    // a forward run left X_T and s1, s2 in the workspace
   std::vector<DynDesc> dyn_cache;
   CallParams call_cache{};
+  // the no-allocation entry point: host image of the workspace's table region
+  // [0, off_scal) (static tables written at plan time, the call's pointer
+  // table per call) and room for the aliasing check, both sized at plan time
+  std::vector<char> image;
+  std::vector<std::pair<uintptr_t, std::pair<uintptr_t, int>>> spans;
 
   size_t elem_bytes() const { return dtype == SLORR_BF16 ? 2 : 4; }     // weights
   size_t grad_bytes() const { return grad_dtype == SLORR_BF16 ? 2 : 4; }  // gradients

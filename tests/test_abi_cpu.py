@@ -396,3 +396,38 @@ def test_null_plan_checks_before_device_use(L):
     assert call(None, 1, w, one, 0, 6, None, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
     lib.slorr_cache_config(L.F32, None)
     assert lib.slorr_cache_clear() == L.OK                   # empty cache: no device call
+
+
+def test_noalloc_checks_before_device_use(L):
+    """slorr_reg_fwd_bwd_noalloc: argument errors, a plan larger than the static
+    scratch and a deferred-gradient plan are refused before any device call."""
+    lib = L.lib()
+    call = lib.slorr_reg_fwd_bwd_noalloc
+    st, h, ws, shapes = _plan(L, [(4, 8), (8, 4)])
+    assert st == L.OK
+    vals = ctypes.c_void_p(0x10000)
+    w = (ctypes.c_void_p * 2)(0x20000, 0x30000)
+    g = (ctypes.c_void_p * 2)(0x40000, 0x50000)
+    assert call(None, 2, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 3, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert call(h, 2, w, shapes, 1, 6, vals, g, 1.0, None) == L.ERR_PLAN_MISMATCH
+    assert call(h, 2, w, shapes, 0, 6, None, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert call(h, 2, w, shapes, 0, 6, vals, None, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    alias = (ctypes.c_void_p * 2)(0x20000, 0x50000)
+    assert call(h, 2, w, shapes, 0, 6, vals, alias, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    lib.slorr_plan_destroy(h)
+    o = L.Options()
+    lib.slorr_default_options(ctypes.byref(o))
+    o.flags = L.DEFER_GRAD
+    st, h, _, shapes = _plan(L, [(4, 8), (8, 4)], opts=o)
+    assert call(h, 2, w, shapes, 0, 6, vals, g, 1.0, None) == L.ERR_INVALID_ARGUMENT
+    assert b"DEFER_GRAD" in lib.slorr_last_error()
+    lib.slorr_plan_destroy(h)
+    big = [(1024, 8192)] * 4                       # > 64 MiB of workspace
+    st, h, ws, shapes = _plan(L, big, L.BF16)
+    assert st == L.OK and ws > (64 << 20)
+    w4 = (ctypes.c_void_p * 4)(*[0x100000000 * (i + 1) for i in range(4)])
+    g4 = (ctypes.c_void_p * 4)(*[0x800000000 + 0x100000000 * i for i in range(4)])
+    assert call(h, 4, w4, shapes, 0, 6, vals, g4, 1.0, None) == L.ERR_WORKSPACE
+    assert b"static scratch" in lib.slorr_last_error()
+    lib.slorr_plan_destroy(h)
