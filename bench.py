@@ -31,7 +31,11 @@ GEMM_OPS = ("gram", "poly", "update", "last")
 
 
 def kernel_instance(op, edge):
-    """Name of the GEMM kernel instance a launch runs: mode and block tile."""
+    """Name of the GEMM kernel instance a launch runs: mode and block tile (the
+    256-tile update and last launches of the fp16 iterate run the persistent
+    kernel k_upd256)."""
+    if op in ("update", "last") and edge == 256:
+        return f"k_upd256<{op}>"
     return f"k_gemm<{op}, {edge}x{edge}>"
 
 

@@ -78,6 +78,7 @@ struct GemmArgs {
   int kap;        // first step: coefficients times powers of the matrix's kappa
   float alpha, beta, gamma, inv_sx;
   float *gpart;   // Gram parts (split K): fp32 partial tiles, BM x BN each, at tile.slot
+  int ntiles;     // entries of the tile list (a persistent kernel's grid can be smaller)
 };
 
 template <int BM, int BN, int WGM, int WGN>
@@ -594,5 +595,376 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
     __syncthreads();                      // the block sum reuses wave 0's staging area
     const double r = block_sum<NT>(tsum, reinterpret_cast<double *>(smem));
     if (tid == 0) args.tpart[tile.slot] = r;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Update / Last of the fp16 iterate on 256 x 256 tiles: a persistent kernel.
+//
+// One block per CU walks the launch's tile list with a stride of the grid
+// size. The grid is a multiple of the XCD count, so every list entry runs on
+// the XCD the list assigns it to, as in a launch of one block per tile.
+//
+// Tile contexts: at the start, lane t of every wave loads what tile t of the
+// block's sequence needs (operand offsets, padded dims, tile coordinates) into
+// a register table, read later with readlane. The main loop then issues no
+// memory access besides the operand fetches, so a slab's wait counts only
+// them (a descriptor load in the loop would need a wait that drains every
+// fetch in flight). A block with more than 64 tiles reloads the table.
+//
+// Operand pipeline: k-slabs of BK in NS LDS stages, fetched NS - 1 slabs
+// ahead. The slab sequence runs on across tiles: the first slabs of the next
+// tile are fetched while the last ones of the current tile are multiplied and
+// while its epilogue runs. A slab is waited for by count (s_waitcnt vmcnt
+// with the fetches issued after it still outstanding; vector loads complete
+// in issue order, and outstanding stores only make the wait longer), then one
+// block barrier publishes it and frees the stage of the previous slab, into
+// which the next fetch goes. LDS: the stages and a separate 32 KB epilogue
+// staging area (4 KB per wave), 160 KB in all (one block per CU).
+//
+// The MFMA operands are swapped with respect to k_gemm: the iterate panel is
+// the instruction's first operand, so each lane's accumulator holds 4
+// consecutive output columns of one row (acc[i][j][4 g + q] = C[row lr of
+// 32-row block i][column 32 j + 8 g + 4 lk + q] of the wave tile). The
+// epilogue scales and rounds them to fp16 and stages them with 8-byte LDS
+// writes; 16-byte reads then give each lane 8 consecutive columns, 8 lanes
+// per row, so the global stores write whole 128-byte row segments. Every
+// output element is the same fp32 sum rounded once, as in k_gemm.
+template <int BK_, int NS_>
+struct Upd256 {
+  static constexpr int BM = 256, BN = 256, WGM = 2, WGN = 4, kWaves = 8, NT = 512;
+  static constexpr int WTM = 128, WTN = 64, FM = 4, FN = 2;
+  static constexpr int BK = BK_;                     // k per slab (32 or 64)
+  static constexpr int NS = NS_;                     // LDS stages (fetch distance NS - 1)
+  static constexpr int KAP = BK * 2;                 // bytes per row of the B stage (K-major)
+  static constexpr int KNP = BN * 2;                 // bytes per k-row of the X stage
+  static constexpr int kStageA = BM * KAP;
+  static constexpr int kStage = kStageA + BK * KNP;
+  static constexpr int kEpi = 32 * 128;              // per wave: 32 rows x 64 fp16
+  static constexpr int kSmem = NS * kStage + kWaves * kEpi;
+  // global -> LDS instructions per wave and slab: B rows (1024 / KAP rows of
+  // KAP bytes each), X rows (2 k-rows of 512 bytes each)
+  static constexpr int RPA = 1024 / KAP;
+  static constexpr int kLoadsA = BM / RPA / kWaves, kLoadsX = BK / 2 / kWaves;
+  static constexpr int kLoads = kLoadsA + kLoadsX;
+  static_assert(BK == 32 || BK == 64, "slab depth");
+  static_assert(NS >= 2 && kSmem <= 160 * 1024, "LDS per CU");
+  static_assert((NS - 2) * kLoads < 64, "vmcnt range");
+};
+
+// Byte offset of 16-byte chunk `chunk` (0..3) of a 64-byte row of the B
+// stage (slabs of 32). The key ((row >> 1) ^ (row >> 3)) & 3 gives any 8
+// consecutive rows 8 distinct (row parity, chunk) pairs (32 banks, 8-lane
+// phase of a 16-byte read) and any 16 consecutive rows 16 distinct (row % 4,
+// chunk) pairs (64 banks, 16-lane phase).
+__device__ __forceinline__ int swz64_key(int row) { return ((row >> 1) ^ (row >> 3)) & 3; }
+__device__ __forceinline__ int swz64(int row, int chunk) { return row * 64 + ((chunk ^ swz64_key(row)) << 4); }
+
+// s_waitcnt vmcnt(N), the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Wait until at most `ahead` (<= A) slabs of fetches, L instructions each,
+// issued by this wave are outstanding.
+template <int L, int A>
+__device__ __forceinline__ void vm_wait_slabs(int ahead) {
+  if constexpr (A >= 2) {
+    if (ahead >= 2) {
+      vm_wait<2 * L>();
+      return;
+    }
+  }
+  if constexpr (A >= 1) {
+    if (ahead >= 1) {
+      vm_wait<L>();
+      return;
+    }
+  }
+  vm_wait<0>();
+}
+
+// Byte offset of 16-byte chunk `chunk` of row `row` of a wave's epilogue
+// staging area (rows of 128 bytes). The key (row >> 1) & 7 gives the 16 rows
+// of an 8-byte write's half-wave distinct (row parity, chunk) pairs, i.e.
+// distinct bank pairs; a 16-byte read's 16-lane phase covers two rows whole.
+__device__ __forceinline__ int epi_off(int row, int chunk) {
+  return row * 128 + ((chunk ^ ((row >> 1) & 7)) << 4);
+}
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(uint32_t(v), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(uint32_t(v >> 32), lane);
+  return (uint64_t(hi) << 32) | lo;
+}
+
+template <int MODE, bool FOLD, int BK, int NS>
+__global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
+  using U = Upd256<BK, NS>;
+  typedef _Float16 T;
+  typedef half8 frag;
+  static_assert(MODE == kUpdate || MODE == kLast, "update kernels only");
+  __shared__ __attribute__((aligned(16))) char smem[U::kSmem];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lk = lane >> 5;
+  const int wm = wave / U::WGN, wn = wave % U::WGN;
+  const int G = gridDim.x;
+  // positions of this block's sequence: entry blockIdx.x + pos * G
+  const int npos = args.ntiles > int(blockIdx.x) ? (args.ntiles - int(blockIdx.x) + G - 1) / G : 0;
+
+  // register table of tile contexts, positions tb .. tb + 63 (lane t: tb + t)
+  int tb = 0;
+  int v_mat, v_tm, v_tn, v_slot, v_pp, v_qp;
+  uint64_t v_a, v_xi, v_xo, v_x0;
+  auto load_table = [&](int base) {
+    tb = base;
+    const int pos = base + lane;
+    v_mat = -1;
+    v_tm = v_tn = v_slot = v_pp = v_qp = 0;
+    v_a = v_xi = v_xo = v_x0 = 0;
+    if (pos < npos) {
+      const Tile t = args.tiles[int(blockIdx.x) + pos * G];
+      v_mat = t.mat;
+      if (t.mat >= 0) {
+        const MatDesc *d = args.mats + t.mat;
+        v_tm = t.tm;
+        v_tn = t.tn;
+        v_slot = t.slot;
+        v_pp = d->Pp;
+        v_qp = d->Qp;
+        v_a = args.use_a ? d->a : d->b;
+        v_xi = d->x[args.xin];
+        v_xo = d->x[args.xout];
+        v_x0 = d->x[0];
+      }
+    }
+  };
+  struct Ctx {
+    const T *Ap, *Bp;   // B (or A) rows, X rows
+    T *Xn;              // output iterate
+    const T *X0;        // X_0' (trace)
+    int ldx, K, m0, n0, mat, slot;
+  };
+  // the first valid position >= pos (npos if none); reloads the table when
+  // pos leaves it
+  auto next_pos = [&](int pos) {
+    for (; pos < npos; ++pos) {
+      if (pos >= tb + 64) load_table(pos);
+      if (__builtin_amdgcn_readlane(v_mat, pos - tb) >= 0) break;
+    }
+    return pos;
+  };
+  auto ctx_at = [&](int pos) {
+    const int t = pos - tb;
+    Ctx c;
+    c.Ap = reinterpret_cast<const T *>(args.ws + readlane64(v_a, t));
+    c.Bp = reinterpret_cast<const T *>(args.ws + readlane64(v_xi, t));
+    c.Xn = reinterpret_cast<T *>(args.ws + readlane64(v_xo, t));
+    c.X0 = reinterpret_cast<const T *>(args.ws + readlane64(v_x0, t));
+    c.ldx = __builtin_amdgcn_readlane(v_qp, t);
+    c.K = __builtin_amdgcn_readlane(v_pp, t);
+    c.m0 = __builtin_amdgcn_readlane(v_tm, t) * U::BM;
+    c.n0 = __builtin_amdgcn_readlane(v_tn, t) * U::BN;
+    c.mat = __builtin_amdgcn_readlane(v_mat, t);
+    c.slot = __builtin_amdgcn_readlane(v_slot, t);
+    return c;
+  };
+
+  // global -> LDS fetch of slab k0 of tile c into stage st: B rows, K-major,
+  // RPA rows of KAP bytes per wave instruction (lane l: row l / (KAP / 16),
+  // physical chunk l % (KAP / 16), fetching the logical chunk the swizzle
+  // puts there); X rows [k][n], 2 k-rows of 512 bytes per wave instruction
+  // in kn_off's layout
+  auto dload = [&](const Ctx &c, int k0, int st) {
+    char *sA = smem + st * U::kStage;
+    char *sB = sA + U::kStageA;
+    constexpr int CPA = U::KAP / 16;
+    const int rsub = lane / CPA, pch = lane % CPA;
+#pragma unroll
+    for (int i = 0; i < U::kLoadsA; ++i) {
+      const int r0 = (wave + i * U::kWaves) * U::RPA, row = r0 + rsub;
+      const int lch = pch ^ (BK == 64 ? swz_key(row) : swz64_key(row));
+      load_lds16(c.Ap + size_t(c.m0 + row) * c.K + k0 + lch * 8, sA + r0 * U::KAP);
+    }
+    constexpr int CPR = U::KNP / 16;
+    const int xsub = lane / CPR, xch = lane % CPR;
+#pragma unroll
+    for (int i = 0; i < U::kLoadsX; ++i) {
+      const int r0 = (wave + i * U::kWaves) * 2, row = r0 + xsub;
+      load_lds16(c.Bp + size_t(k0 + row) * c.ldx + c.n0 + (xch ^ ((row & 3) << 2)) * 8, sB + r0 * U::KNP);
+    }
+  };
+
+  floatx16 acc[U::FM][U::FN];
+  // fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s
+  // run; the X fragment is the instruction's first operand
+  auto compute = [&](int st) {
+    const char *sA = smem + st * U::kStage;
+    const char *sB = sA + U::kStageA;
+    frag fa[2][U::FM], fb[2][U::FN];
+    auto read = [&](int s, int slot) {
+#pragma unroll
+      for (int i = 0; i < U::FM; ++i) {
+        const int row = wm * U::WTM + i * 32 + lr;
+        fa[slot][i] = *reinterpret_cast<const frag *>(sA + (BK == 64 ? swz(row, 2 * s + lk) : swz64(row, 2 * s + lk)));
+      }
+#pragma unroll
+      for (int j = 0; j < U::FN; ++j) {
+        // lane L: k = 16 s + 8 (L / 32) + 0..7 of column n = L % 32 of the
+        // fragment, as two transposing reads of 4 k-rows each
+        const int g = lane >> 4, si = lane & 15;
+        const int row = 16 * s + 8 * (g >> 1) + (si >> 2);
+        const int col = wn * U::WTN + j * 32 + 16 * (g & 1) + 4 * (si & 3);
+        const int off = kn_off(row, col >> 3, U::KNP) + 8 * (si & 1);
+        const half4 lo = lds_read_tr16(sB + off);
+        const half4 hi = lds_read_tr16(sB + off + 4 * U::KNP);
+        fb[slot][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    };
+    read(0, 0);
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      if (s + 1 < BK / 16) read(s + 1, (s + 1) & 1);
+#pragma unroll
+      for (int i = 0; i < U::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < U::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[s & 1][j], fa[s & 1][i], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  load_table(0);
+  int pos = next_pos(0);
+  if (pos >= npos) return;
+  Ctx cur = ctx_at(pos);
+
+  // producer: the next slab to fetch (position ppos, context pc, slab pk);
+  // nextc: the context of the tile after the consumer's
+  static_assert(NS - 1 < kBigTile / BK, "the fetches run at most one tile ahead");
+  int ppos = pos, pk = 0, npos_c = pos;   // npos_c: position of nextc
+  Ctx pc = cur, nextc = cur;
+  bool pvalid = true;
+  int issued = 0;                      // slabs fetched so far
+  auto produce = [&](int st) {
+    if (!pvalid) return;
+    dload(pc, pk * BK, st);
+    ++issued;
+    if (++pk == pc.K / BK) {
+      ppos = next_pos(ppos + 1);
+      pvalid = ppos < npos;
+      if (pvalid) {
+        pc = ctx_at(ppos);
+        nextc = pc;
+        npos_c = ppos;
+      }
+      pk = 0;
+    }
+  };
+#pragma unroll
+  for (int q = 0; q < NS - 1; ++q) produce(q);
+
+  char *ep = smem + NS * U::kStage + wave * U::kEpi;
+  // Last: the X_0' values of the trace, 8 consecutive columns per lane in
+  // the epilogue's read-back layout, loaded two 32-row blocks ahead
+  half8 x0v[MODE == kLast ? 2 : 1][4];
+  auto x0load = [&](const Ctx &c, int i) {
+    if constexpr (MODE == kLast) {
+      const int row_w = c.m0 + wm * U::WTM, col_w = c.n0 + wn * U::WTN;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int q = lane + 64 * t, row = q >> 3, ch = q & 7;
+        x0v[i & 1][t] = *reinterpret_cast<const half8 *>(c.X0 + size_t(row_w + i * 32 + row) * c.ldx + col_w + 8 * ch);
+      }
+    }
+  };
+  int g = 0;                           // slab being multiplied (global count)
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < U::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < U::FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+    // K is a multiple of 256 (padding), so of BK
+    const int nk = cur.K / BK;
+    for (int kt = 0; kt < nk; ++kt, ++g) {
+      vm_wait_slabs<U::kLoads, NS - 2>(issued - g - 1);   // slab g has landed (this wave's part)
+      __syncthreads();                 // ... every wave's part; slab g - 1 is done
+      produce((g + NS - 1) % NS);
+      compute(g % NS);
+    }
+
+    // ---------------------------------------------------------- epilogue
+    float alpha = args.alpha, beta = args.beta;
+    if (args.kap) {                        // first (cubic) step: kappa^3 a, kappa b
+      const double kp = args.sc[cur.mat].kappa;
+      alpha = float(double(args.alpha) * kp * kp * kp);
+      beta = float(double(args.beta) * kp);
+    }
+    const int row_w = cur.m0 + wm * U::WTM, col_w = cur.n0 + wn * U::WTN;
+    double tsum = 0.0;
+    x0load(cur, 0);
+    x0load(cur, 1);
+#pragma unroll
+    for (int i = 0; i < U::FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < U::FN; ++j)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float v[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * q4 + q];
+          if constexpr (FOLD) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] *= alpha;
+          } else {
+            const half4 in = *reinterpret_cast<const half4 *>(
+                cur.Bp + size_t(row_w + i * 32 + lr) * cur.ldx + col_w + 32 * j + 8 * q4 + 4 * lk);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = beta * float(in[q]) + alpha * v[q];
+          }
+          half4 h;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) h[q] = _Float16(v[q]);
+          *reinterpret_cast<half4 *>(ep + epi_off(lr, 4 * j + q4) + 8 * lk) = h;
+        }
+      // the staging area is the wave's own and one wave's LDS operations are
+      // performed in order: a wave-level barrier (no reordering) suffices
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int c = lane + 64 * t, row = c >> 3, ch = c & 7;
+        const half8 h = *reinterpret_cast<const half8 *>(ep + epi_off(row, ch));
+        const size_t o = size_t(row_w + i * 32 + row) * cur.ldx + col_w + 8 * ch;
+        if (MODE == kUpdate || args.write_x) __builtin_nontemporal_store(h, reinterpret_cast<half8 *>(cur.Xn + o));
+        if constexpr (MODE == kLast) {
+          // P as stored times X_0' (both in the iterate's scale): the
+          // products of two fp16 values are exact in fp64
+#pragma unroll
+          for (int q = 0; q < 8; ++q) tsum += double(h[q]) * double(x0v[i & 1][t][q]);
+        }
+      }
+      if (i + 2 < U::FM) x0load(cur, i + 2);
+      __builtin_amdgcn_wave_barrier();
+    }
+    if constexpr (MODE == kLast) {
+      // per-tile partial of the trace: waves in order, each a fixed butterfly
+      const double w = wave_sum(tsum);
+      if (lane == 0) *reinterpret_cast<double *>(ep) = w;
+      __syncthreads();
+      if (tid == 0) {
+        double r = 0.0;
+        for (int q = 0; q < U::kWaves; ++q)
+          r += *reinterpret_cast<const double *>(smem + NS * U::kStage + q * U::kEpi);
+        args.tpart[cur.slot] = r;
+      }
+    }
+    if (npos_c == pos) break;          // the fetches found no further tile
+    pos = npos_c;
+    cur = nextc;
   }
 }

@@ -29,6 +29,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <mutex>
 #include <stdexcept>
 #include <string>
@@ -531,11 +532,39 @@ void go(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s, const Ev
     hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
 }
 
+// Slab depth and LDS stages of the persistent update kernel (64-deep slabs
+// in two stages measured faster than 32-deep ones in three or four).
+constexpr int kUpdBK = 64, kUpdNS = 2;
+
+// Grid of a persistent kernel over `entries` tile-list entries: one block per
+// CU, rounded down to a multiple of the XCD count (entry e then runs on XCD
+// e % kXcds, as with one block per entry); never more blocks than entries.
+int persistent_grid(int entries) {
+  static std::mutex mu;
+  static int cus[64];
+  int dev = 0;
+  check(hipGetDevice(&dev), "hipGetDevice");
+  int n;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    if (dev < 0 || dev >= 64) throw HipError("device index out of range");
+    if (!cus[dev]) {
+      int c = 0;
+      check(hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
+      cus[dev] = std::max(kXcds, c - c % kXcds);
+    }
+    n = cus[dev];
+  }
+  return entries < n ? entries : n;
+}
+
 template <typename Tx, typename Tw, int BM, int BN, int WGM, int WGN>
 void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPair *ev) {
   const dim3 block(GemmShape<BM, BN, WGM, WGN>::kThreads);
   // the planner gives fp32 sets 128-tiles for the update launches
   constexpr bool kUpd = sizeof(Tx) == 2 || BM == kTile;
+  // fp16 iterate, 256-tiles: the persistent update kernel
+  constexpr bool kPersist = sizeof(Tx) == 2 && BM == kBigTile && BN == kBigTile;
   switch (op) {
     case Op::Gram:
       go(k_gemm<Tx, Tw, kGram, BM, BN, WGM, WGN>, grid, block, s, ev, a);
@@ -544,11 +573,19 @@ void launch_gemm(Op op, dim3 grid, const GemmArgs &a, hipStream_t s, const EvPai
       go(k_gemm<Tx, Tw, kPoly, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       break;
     case Op::Update:
-      if constexpr (kUpd) go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      if constexpr (kPersist) {
+        if (a.fold) go(k_upd256<kUpdate, true, kUpdBK, kUpdNS>, dim3(persistent_grid(a.ntiles)), block, s, ev, a);
+        else go(k_upd256<kUpdate, false, kUpdBK, kUpdNS>, dim3(persistent_grid(a.ntiles)), block, s, ev, a);
+      }
+      else if constexpr (kUpd) go(k_gemm<Tx, Tw, kUpdate, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       else throw HipError("no fp32 256-tile update kernel");
       break;
     default:
-      if constexpr (kUpd) go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
+      if constexpr (kPersist) {
+        if (a.fold) go(k_upd256<kLast, true, kUpdBK, kUpdNS>, dim3(persistent_grid(a.ntiles)), block, s, ev, a);
+        else go(k_upd256<kLast, false, kUpdBK, kUpdNS>, dim3(persistent_grid(a.ntiles)), block, s, ev, a);
+      }
+      else if constexpr (kUpd) go(k_gemm<Tx, Tw, kLast, BM, BN, WGM, WGN>, grid, block, s, ev, a);
       else throw HipError("no fp32 256-tile update kernel");
       break;
   }
@@ -615,6 +652,7 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev,
         a.gamma = l.gamma;
         a.inv_sx = 1.0f / sx;
         a.gpart = reinterpret_cast<float *>(ws + p.off_gpart);
+        a.ntiles = l.grid;
         if (l.cfg == kCfg256)
           launch_gemm<Tx, Tw, kBigTile, kBigTile, 2, 4>(l.op, grid, a, s, ev);
         else

@@ -50,6 +50,20 @@ def test_vit_b16(kind):
     compare(vals, grads, refs, kind, cfg.dtype, label="vit_b16")
 
 
+def test_vit_b16_cubic():
+    """Degree 3 schedule on the benchmarked set: the large-tile update kernels
+    take the path without the folded identity term (X' = a X + b A X, the
+    a X term read back in the epilogue, kappa applied per matrix in the first
+    step). The GPU runs the whole set; a block of matrices is compared."""
+    cfg = CONFIGS["vit_b16"]
+    arrs = make_set("vit_b16", 0)
+    vals, grads, _ = run_gpu(arrs, cfg.dtype, "hoyer", 8, degree=3, eps=1e-4)
+    idx = [0, 1, 2, 3, 45, 46, 47]
+    refs = run_oracle([arrs[i] for i in idx], cfg.dtype, "hoyer", 8, eps=1e-4, table=default_table(8, d=3))
+    compare(np.array([vals[i] for i in idx] + [0.0]), [grads[i] for i in idx], refs, "hoyer", cfg.dtype,
+            label="vit_b16 cubic", check_total=False)
+
+
 # ------------------------------------------------- the large sets, every matrix
 # One GPU run per (set, kind), kept as fp32 gradients; the oracle comparison is
 # split into parts of a few blocks, each a test of its own (with progress).

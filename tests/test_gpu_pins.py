@@ -211,3 +211,33 @@ def test_null_plan_uses_the_plan_cache():
             assert torch.equal(a, b), rep
     lib.slorr_cache_config(L.F32, None)
     assert lib.slorr_cache_clear() == L.OK
+
+
+def test_large_set_matches_subset_bitwise():
+    """A matrix's results do not depend on the rest of the set when every
+    launch uses the same kernel configuration: 17 matrices of 4096 x 16384
+    (17408 update tiles, more than 64 per block of the persistent update
+    kernel, so each block reloads its tile table) against the first 4 alone
+    (4096 tiles), both with 256-tiles in every GEMM launch; values and
+    gradients bit for bit. Weights are drawn on the device (no oracle)."""
+    import torch
+    from paper_2607_08754_amd import Plan
+    shape = (4096, 16384)
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(1234)
+    W = [(torch.randn(shape, generator=gen, device="cuda:0") * 0.02).to(torch.bfloat16) for _ in range(17)]
+    out, edges = {}, {}
+    for n in (17, 4):
+        plan = Plan([shape] * n, dtype="bf16", kind="hoyer", iters=6, eps=1e-4, device="cuda:0")
+        edges[n] = [(op, te) for op, _, te in plan.launches()]
+        G = [torch.empty(shape, dtype=torch.float32, device="cuda:0") for _ in range(4)]
+        G += [torch.empty(shape, dtype=torch.float32, device="cuda:0") for _ in range(n - 4)]
+        vals = plan(W[:n], G)
+        torch.cuda.synchronize()
+        out[n] = (vals[:4].cpu(), G[:4])
+        plan.close()
+        print(f"[pins] 4096x16384 set of {n}: values {out[n][0].tolist()}", flush=True)
+    assert edges[17] == edges[4] and all(te == 256 for op, te in edges[4] if te), edges[4]
+    assert torch.equal(out[17][0], out[4][0])
+    for a, b in zip(out[17][1], out[4][1]):
+        assert torch.equal(a, b)
