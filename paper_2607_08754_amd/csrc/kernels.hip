@@ -13,10 +13,12 @@
 //                Poly    B = b A + c A A + a I      (A symmetric: A A = A A^T)
 //                                                   (first step: kappa a, kappa^3 b,
 //                                                   kappa^5 c)
-//                Update  X' = B X                   (B symmetric)
-//                Last    X_T = a X + B X with the trace partials of
-//                        sum(W * P), P = X_T (Sec. 3 "Computing the nuclear
-//                        and Frobenius norms")
+//                Update  X' = B X                   (B symmetric; k_upd256 for
+//                                                   the fp16 iterate on 256-tiles)
+//                Last    X_T = B X with the per-tile partials of the trace
+//                        sum(X_0' * P), P = X_T as stored; 2^e times it is
+//                        sum(W * P) (Sec. 3 "Computing the nuclear and
+//                        Frobenius norms")
 //   k_finalize values L_i and gradient factors, one block per matrix
 //              (Sec. 3 definitions; Eq. SLORR_grads; Listing 1)
 //   k_setsum   the set total in index order (Sec. 3, L summed over the set)
