@@ -182,32 +182,54 @@ __device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const Mat
   }
 }
 
-// ||W||_F^2 partial of one canonical 64 x 64 tile, fp64: thread q adds the
-// squares of canonical row q / 8, columns 8 (q % 8) .. + 7, in column order,
-// then the block sums in thread order. The order depends only on the
-// canonical tile, so W and W^T give bitwise equal partials.
+// ||W||_F^2 partial of one canonical 64 x 64 tile, fp64, one wave per tile
+// (four tiles per block): lane q takes the canonical 8 x 8 block (q / 8,
+// q % 8) and reads it as eight 8-element row pieces of W straight from
+// global memory (a row of W is a canonical row of a wide W and a canonical
+// column of a tall one, so both orientations read whole row pieces, 8 lanes
+// covering 64 consecutive elements of a row); it adds the 64 squares in
+// canonical row-major order, then the wave sums the lanes with a fixed
+// butterfly. The order depends only on the canonical tile, so W and W^T give
+// bitwise equal partials.
 template <typename Tw>
 __global__ __launch_bounds__(kThreads) void k_sumsq(const Tile *__restrict__ tiles,
                                                     const MatDesc *__restrict__ mats,
                                                     const DynDesc *__restrict__ dyn,
-                                                    double *__restrict__ part) {
-  __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
-  __shared__ double sh[kThreads / 64];
-  const Tile t = tiles[blockIdx.x];
+                                                    double *__restrict__ part, int ntiles) {
+  const int e = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (e >= ntiles) return;                       // whole wave
+  const int lane = threadIdx.x & 63;
+  const Tile t = tiles[e];
   const MatDesc d = mats[t.mat];
-  stage_tile(tile, t, d, static_cast<const Tw *>(dyn[t.mat].w), 1.0f);
-  __syncthreads();
-  double acc = 0.0;
-  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
-    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+  const Tw *w = static_cast<const Tw *>(dyn[t.mat].w);
+  // the block's corner in the canonical tile: row cm, column cn; the rows of
+  // W it reads start at r0 (wide: canonical rows, tall: canonical columns)
+  const int cm = t.tm * kPrepTile + 8 * (lane >> 3), cn = t.tn * kPrepTile + 8 * (lane & 7);
+  const int r0 = d.tall ? cn : cm, c0 = d.tall ? cm : cn;
+  const int nv = max(0, min(8, d.cols - c0));
+  float v[8][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const double x = tile[r * kPrepPitch + c + j];
-      acc += x * x;
-    }
+  for (int a = 0; a < 8; ++a) get8(w + size_t(r0 + a) * d.cols + c0, r0 + a < d.rows ? nv : 0, v[a]);
+  double acc = 0.0;
+  if (!d.tall) {
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const double x = v[a][b];                // canonical (cm + a, cn + b)
+        acc += x * x;
+      }
+  } else {
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int b = 0; b < 8; ++b) {
+        const double x = v[b][a];                // canonical (cm + a, cn + b) = W (cn + b, cm + a)
+        acc += x * x;
+      }
   }
-  const double r = block_sum<kThreads>(acc, sh);
-  if (threadIdx.x == 0) part[t.slot] = r;
+  acc = wave_sum(acc);
+  if (lane == 0) part[t.slot] = acc;
 }
 
 // f, f + eps, kappa and the X_0 scale per matrix: one wave per matrix sums its
@@ -624,7 +646,8 @@ void launch_one(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev,
     const dim3 grid(l.grid), block(kThreads);
     switch (l.op) {
       case Op::SumSq:
-        go(k_sumsq<Tw>, grid, block, s, ev, tiles + l.tile_first, mats, dyn, sumsq);
+        go(k_sumsq<Tw>, dim3((l.grid + kThreads / 64 - 1) / (kThreads / 64)), block, s, ev, tiles + l.tile_first, mats,
+           dyn, sumsq, l.grid);                    // l.grid: tiles, one wave each
         break;
       case Op::NormFin:
         go(k_norm_fin, grid, block, s, ev, mats, sc, sumsq, p.n, p.eps, sx);   // 4 matrices per block
