@@ -334,6 +334,32 @@ def test_graph_equals_eager_and_determinism(dtype):
             assert np.array_equal(a, b)
 
 
+def test_benchmarked_set_is_deterministic():
+    """The benchmarked set (persistent update kernel, XCD-ordered tile lists,
+    fixed-order reductions): five graph replays and one launch-by-launch call
+    give bitwise equal values and gradients."""
+    import torch
+    from paper_2607_08754_amd import Plan
+    cfg = CONFIGS["vit_b16"]
+    W = to_device(make_set("vit_b16", 0), cfg.dtype, "cuda:0")
+    G = [torch.empty(s, dtype=torch.float32, device="cuda:0") for s in cfg.shapes]
+    plan = Plan(cfg.shapes, dtype=cfg.dtype, kind="hoyer", iters=cfg.iters, device="cuda:0")
+    outs = []
+    for rep in range(6):
+        if rep < 5:
+            v = plan(W, G)
+        else:
+            v, _ = plan.profiled(W, G)
+        torch.cuda.synchronize()
+        outs.append((v.cpu().numpy(), [g[:64, :64].cpu().numpy() for g in G], float(sum(g.double().sum() for g in G))))
+    plan.close()
+    for v, gs, tot in outs[1:]:
+        assert np.array_equal(v, outs[0][0])
+        assert tot == outs[0][2]
+        for a, b in zip(gs, outs[0][1]):
+            assert np.array_equal(a, b)
+
+
 def test_pointer_change_between_calls():
     """New weight / gradient tensors between replays of one plan."""
     import torch
