@@ -19,6 +19,12 @@ constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 constexpr int64_t kMinBigTiles = 2 * kCus;  // two 256-tiles per CU
 constexpr int64_t kMinGramUnits = 2 * kCus; // Gram blocks wanted per launch (two per CU)
 constexpr int kMaxGramParts = 16;           // k parts per Gram tile at most
+// split only Gram tiles this many k-slabs long, into parts of at least this
+// many slabs: fp16 slabs (64 values of k) are bound by their load latency
+// (about 0.7 us on a 128-tile), fp32 slabs (32 values) by the fp32 MFMA rate
+// (about 1.7 us), and a reduce launch costs about 7 us
+constexpr int kMinSplitSlabs16 = 32, kMinPartSlabs16 = 8;
+constexpr int kMinSplitSlabs32 = 8, kMinPartSlabs32 = 4;
 
 Tile make_tile(int32_t mat, int32_t tm, int32_t tn, int32_t slot) {
   Tile t{};
@@ -219,17 +225,27 @@ void build_plan(Plan &p) {
   p.gsplit = TileRange{};
   p.gred = TileRange{};
   p.gram_parts = 0;
-  if (p.gram[kCfg256].count == 0) {
+  // The parts and the reduce launch cost more than they save unless the
+  // tiles are long: only sets whose longest Gram tile has enough k-slabs of
+  // the kernel (64 fp16 / 32 fp32 values of k) are split, into parts of a
+  // minimum number of slabs.
+  const int slab_k = f16 ? 64 : 32;
+  const int kMinSplitSlabs = f16 ? kMinSplitSlabs16 : kMinSplitSlabs32;
+  const int kMinPartSlabs = f16 ? kMinPartSlabs16 : kMinPartSlabs32;
+  int max_slabs = 0;
+  for (int i : order) max_slabs = std::max(max_slabs, p.mats[i].Qp / slab_k);
+  if (p.gram[kCfg256].count == 0 && max_slabs >= kMinSplitSlabs) {
     int64_t ntiles = 0;
     for (int i : order) ntiles += int64_t(p.mats[i].Pp / kTile) * (p.mats[i].Pp / kTile + 1) / 2;
     if (ntiles > 0 && ntiles < kMinGramUnits) {
       const int want = int(std::max<int64_t>(1, std::min<int64_t>(kMaxGramParts, kMinGramUnits / ntiles)));
+      const int per_min = std::max(1, kMinPartSlabs * slab_k / kTile);   // k blocks of kTile per part
       std::vector<Job> jobs;
       std::vector<Tile> reds;
       for (int i : order) {
         const MatDesc &d = p.mats[i];
         const int nblk = d.Qp / kTile;                     // k blocks of kTile
-        const int per = (nblk + std::min(want, nblk) - 1) / std::min(want, nblk);
+        const int per = std::max(per_min, (nblk + std::min(want, nblk) - 1) / std::min(want, nblk));
         const int parts = (nblk + per - 1) / per;
         Job j{i, double(per * kTile), {}};
         const int nt = d.Pp / kTile;

@@ -91,11 +91,16 @@ def _expected_mfma(shapes, T):
     return T * sum(2 * _tri(P, tg) * Q + 2 * _tri(P, tp) * P + 2.0 * P * P * Q for P, Q in mats)
 
 
-def _split_k(shapes):
-    """Whether the Gram launch is split into k parts (128-tiles, fewer than 512)."""
+def _split_k(shapes, dtype="bf16"):
+    """Whether the Gram launch is split into k parts: 128-tiles, fewer than
+    512 of them, and a longest tile of at least 32 k-slabs of 64 values of k
+    (the fp16 iterate of bf16 sets) or 8 k-slabs of 32 values (fp32 sets)."""
     mats = [(_pad(min(s)), _pad(max(s))) for s in shapes if min(s) > 0]
     big = sum((P // 256) * (P // 256 + 1) // 2 for P, _ in mats)
     if mats and all(P % 256 == 0 for P, _ in mats) and big >= 256:
+        return False
+    slab, need = (64, 32) if dtype == "bf16" else (32, 8)
+    if not mats or max(Q for _, Q in mats) // slab < need:
         return False
     n128 = sum((P // 128) * (P // 128 + 1) // 2 for P, _ in mats)
     return 0 < n128 < 512
@@ -119,7 +124,7 @@ def test_plan_facts(L, name):
     assert info.groups == len({(min(s), max(s)) for s in cfg.shapes})
     # sumsq, norm, prep; per step the Gram (+ its reduce when split), the poly
     # and the update; finalize, set sum, grad
-    per_step = 4 if _split_k(cfg.shapes) else 3
+    per_step = 4 if _split_k(cfg.shapes, cfg.dtype) else 3
     assert info.launches == 3 + per_step * cfg.iters + 3
     assert info.workspace_bytes == ws > 0
     esz = 2 if cfg.dtype == "bf16" else 4
@@ -345,9 +350,10 @@ def test_deferred_gradient_and_apply_checks_before_device_use(L):
 
 
 def test_split_k_gram_plan(L):
-    """A set with few Gram tiles gets split-K Gram parts plus a reduce launch
-    in every step; the parts cover every k exactly once (same executed MFMA
-    work as one pass per tile). Sets with enough tiles are not split."""
+    """A set with few but long Gram tiles gets split-K Gram parts plus a
+    reduce launch in every step; the parts cover every k exactly once (same
+    executed MFMA work as one pass per tile). Sets with enough tiles, or with
+    short ones, are not split."""
     def facts(shapes):
         st, h, _, _ = _plan(L, shapes, L.BF16, L.HOYER)
         assert st == L.OK
@@ -356,7 +362,7 @@ def test_split_k_gram_plan(L):
         L.lib().slorr_plan_destroy(h)
         return info
     T = 6
-    for shapes in ([(384, 640), (640, 384), (256, 384)], [(256, 4096), (4096, 256), (384, 2944)]):
+    for shapes in ([(384, 2048), (2048, 384), (256, 2304)], [(256, 4096), (4096, 256), (384, 2944)]):
         assert _split_k(shapes)
         info = facts(shapes)
         assert info.launches == 3 + 4 * T + 3                # gram parts, reduce, poly, update
@@ -364,6 +370,9 @@ def test_split_k_gram_plan(L):
     big = facts(CONFIGS["vit_b16"].shapes)
     assert not _split_k(CONFIGS["vit_b16"].shapes)
     assert big.launches == 3 + 3 * T + 3
+    short = [(384, 640), (640, 384), (256, 384)]         # few tiles, but short: one pass
+    assert not _split_k(short)
+    assert facts(short).launches == 3 + 3 * T + 3
 
 
 def test_null_plan_checks_before_device_use(L):
