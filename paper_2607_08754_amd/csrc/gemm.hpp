@@ -642,10 +642,14 @@ struct Upd256 {
   static constexpr int kStage = kStageA + BK * KNP;
   static constexpr int kEpi = 32 * 128;              // per wave: 32 rows x 64 fp16
   static constexpr int kSmem = NS * kStage + kWaves * kEpi;
-  // global -> LDS instructions per wave and slab: B rows (1024 / KAP rows of
-  // KAP bytes each), X rows (2 k-rows of 512 bytes each)
+  // global -> LDS instructions per fetching wave and slab: B rows (1024 / KAP
+  // rows of KAP bytes each), X rows (2 k-rows of 512 bytes each). Only the
+  // first kFetchWaves waves fetch (one per SIMD): a wave stalls while its
+  // fetches wait for the address unit, and the other wave of its SIMD keeps
+  // the MFMA pipe busy meanwhile.
+  static constexpr int kFetchWaves = 4;
   static constexpr int RPA = 1024 / KAP;
-  static constexpr int kLoadsA = BM / RPA / kWaves, kLoadsX = BK / 2 / kWaves;
+  static constexpr int kLoadsA = BM / RPA / kFetchWaves, kLoadsX = BK / 2 / kFetchWaves;
   static constexpr int kLoads = kLoadsA + kLoadsX;
   static_assert(BK == 32 || BK == 64, "slab depth");
   static_assert(NS >= 2 && kSmem <= 160 * 1024, "LDS per CU");
@@ -779,23 +783,33 @@ __global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
   // physical chunk l % (KAP / 16), fetching the logical chunk the swizzle
   // puts there); X rows [k][n], 2 k-rows of 512 bytes per wave instruction
   // in kn_off's layout
+  // (one running address per operand: successive instructions of a wave are
+  // a fixed number of rows apart, and the swizzle key repeats over them)
+  static_assert((U::kFetchWaves * U::RPA) % 32 == 0 && (U::kFetchWaves * 2) % 4 == 0, "swizzle period");
   auto dload = [&](const Ctx &c, int k0, int st) {
+    if (wave >= U::kFetchWaves) return;
     char *sA = smem + st * U::kStage;
     char *sB = sA + U::kStageA;
     constexpr int CPA = U::KAP / 16;
     const int rsub = lane / CPA, pch = lane % CPA;
-#pragma unroll
-    for (int i = 0; i < U::kLoadsA; ++i) {
-      const int r0 = (wave + i * U::kWaves) * U::RPA, row = r0 + rsub;
+    {
+      const int row = wave * U::RPA + rsub;
       const int lch = pch ^ (BK == 64 ? swz_key(row) : swz64_key(row));
-      load_lds16(c.Ap + size_t(c.m0 + row) * c.K + k0 + lch * 8, sA + r0 * U::KAP);
+      const T *pa = c.Ap + size_t(c.m0 + row) * c.K + k0 + lch * 8;
+      const size_t step = size_t(U::kFetchWaves * U::RPA) * c.K;
+#pragma unroll
+      for (int i = 0; i < U::kLoadsA; ++i, pa += step)
+        load_lds16(pa, sA + (wave + i * U::kFetchWaves) * U::RPA * U::KAP);
     }
     constexpr int CPR = U::KNP / 16;
     const int xsub = lane / CPR, xch = lane % CPR;
+    {
+      const int row = wave * 2 + xsub;
+      const T *px = c.Bp + size_t(k0 + row) * c.ldx + c.n0 + (xch ^ ((row & 3) << 2)) * 8;
+      const size_t step = size_t(U::kFetchWaves * 2) * c.ldx;
 #pragma unroll
-    for (int i = 0; i < U::kLoadsX; ++i) {
-      const int r0 = (wave + i * U::kWaves) * 2, row = r0 + xsub;
-      load_lds16(c.Bp + size_t(k0 + row) * c.ldx + c.n0 + (xch ^ ((row & 3) << 2)) * 8, sB + r0 * U::KNP);
+      for (int i = 0; i < U::kLoadsX; ++i, px += step)
+        load_lds16(px, sB + (wave + i * U::kFetchWaves) * 2 * U::KNP);
     }
   };
 
