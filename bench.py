@@ -112,12 +112,13 @@ def _code_only(text):
 
 def _kernels_hash(read=None):
     """Hash of the library's sources (kernels and the plan that orders their
-    tiles), comments left out: a traffic record stays valid across comment
-    edits and goes stale with any change of code."""
+    tiles; not the diagnostic probe programs), comments left out: a traffic
+    record stays valid across comment edits and goes stale with any change of
+    code."""
     csrc = os.path.join(ROOT, "paper_2607_08754_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".hpp", ".cpp", ".h")):
+        if name.endswith((".hip", ".hpp", ".cpp", ".h")) and not name.startswith("probe_"):
             if read is None:
                 with open(os.path.join(csrc, name), encoding="utf-8") as f:
                     text = f.read()

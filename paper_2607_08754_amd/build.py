@@ -1,9 +1,11 @@
 """Build libslorr.so (HIP for gfx950 + host C++) in-tree with hipcc.
 
-    python -m paper_2607_08754_amd.build
+    python -m paper_2607_08754_amd.build            # the library
+    python -m paper_2607_08754_amd.build --probe    # + the main-loop ceiling probe
 
 Objects go to paper_2607_08754_amd/_build/, the library to
-paper_2607_08754_amd/libslorr.so (replaced atomically).
+paper_2607_08754_amd/libslorr.so (replaced atomically), the diagnostic
+program csrc/probe_ceiling.hip to paper_2607_08754_amd/probe_ceiling.
 """
 from __future__ import annotations
 
@@ -19,6 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libslorr.so")
+PROBE = os.path.join(PKG, "probe_ceiling")
 
 SOURCES = ["kernels.hip", "api.cpp", "plan.cpp", "pe_schedule.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -77,6 +80,19 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def build_probe(verbose: bool = False) -> str:
+    cmd = [HIPCC, *COMMON, os.path.join(CSRC, "probe_ceiling.hip"), "-o", PROBE + ".tmp"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"hipcc failed on probe_ceiling.hip:\n{res.stdout}\n{res.stderr}")
+    os.replace(PROBE + ".tmp", PROBE)
+    if verbose:
+        print(f"built {PROBE}")
+    return PROBE
+
+
 if __name__ == "__main__":
     build(verbose=True)
+    if "--probe" in sys.argv[1:]:
+        build_probe(verbose=True)
     sys.exit(0)

@@ -1,0 +1,215 @@
+// Main-loop ceiling of the 256x256 fp16 update tile on gfx950: a diagnostic
+// program, not part of the library. Every block runs the update kernel's k
+// loop (64-deep slabs, two LDS stages, one barrier per slab) over 48 slabs of
+// L2-resident operands, with parts of the loop switched on step by step:
+//
+//   MFMA only         fragments read once, then only MFMAs and the barrier
+//   + LDS reads       the fragment reads of each k step (row operand by
+//                     16-byte reads, [k][n] operand by ds_read_b64_tr_b16)
+//   + fetches         the next slab's operands fetched global -> LDS
+//   fetches to VGPRs  as "+ fetches", but the same bytes are loaded into
+//                     registers and discarded: no LDS write at all
+//
+// for the production layout (8 waves of 128x64) and for 4 waves of 128x128
+// (a third fewer LDS bytes per MFMA). Wave 0 of each block also reads the
+// shader clock counter and the constant-rate wall clock at its start and end,
+// so the output gives the clock the chip ran at under that load next to the
+// MFMA rate. The clock depends on the operand values (the power drawn by the
+// matrix cores grows with the bits they switch), so every variant runs twice:
+// on zero operands and on uniform random fp16 values in [-1, 1), which switch
+// like a Polar Express iterate does.
+//
+//   python -m paper_2607_08754_amd.build --probe
+//   paper_2607_08754_amd/probe_ceiling
+#include "kernels.hip"
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#define CK(x)                                                                                    \
+  do {                                                                                           \
+    hipError_t e_ = (x);                                                                         \
+    if (e_ != hipSuccess) {                                                                      \
+      fprintf(stderr, "%s:%d %s\n", __FILE__, __LINE__, hipGetErrorString(e_));                  \
+      exit(2);                                                                                   \
+    }                                                                                            \
+  } while (0)
+
+namespace slorr {
+
+constexpr int kK = 768, kLdx = 3072;   // operand extents: A is kK x kK, X is kK x kLdx
+
+// MODE 0: MFMA only; 1: + LDS fragment reads; 2: + global -> LDS fetches;
+// 3: MODE 1 + the fetches' loads into registers (no LDS write).
+template <int MODE, int NW>
+__global__ __launch_bounds__(NW * 64) void k_ceiling(unsigned long long *clk, const _Float16 *A,
+                                                     const _Float16 *X, int nslab) {
+  constexpr int WTM = 128, WTN = NW == 8 ? 64 : 128, FM = 4, FN = WTN / 32, WGN = 256 / WTN;
+  constexpr int KNP = 512, kA = 256 * 128, kStage = kA + 64 * KNP;
+  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lr = lane & 31, lk = lane >> 5;
+  const int wm = wave / WGN, wn = wave % WGN;
+  const unsigned long long c0 = clock64(), w0 = wall_clock64();
+  // tile of this block inside the operands: rows m0 of A, columns n0 of X
+  const int m0 = (blockIdx.x % 3) * 256, n0 = (blockIdx.x / 3 % 12) * 256;
+  auto fetch = [&](int k0, int buf) {
+    char *sA = smem + buf * kStage, *sB = sA + kA;
+    const int rsub = lane >> 3, pch = lane & 7;
+#pragma unroll
+    for (int i = 0; i < 32 / NW; ++i) {   // 256 rows of 128 bytes, 8 rows per instruction
+      const int r0 = (wave + i * NW) * 8, row = r0 + rsub;
+      load_lds16(A + size_t(m0 + row) * kK + k0 + (pch ^ swz_key(row)) * 8, sA + r0 * 128);
+    }
+    const int xsub = lane >> 5, xch = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 32 / NW; ++i) {   // 64 rows of 512 bytes, 2 rows per instruction
+      const int r0 = (wave + i * NW) * 2, row = r0 + xsub;
+      load_lds16(X + size_t(k0 + row) * kLdx + n0 + (xch ^ ((row & 3) << 2)) * 8, sB + r0 * KNP);
+    }
+  };
+  half8 fa[2][FM], fb[2][FN];
+  auto read = [&](const char *sA, const char *sB, int s, int slot) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      fa[slot][i] = *reinterpret_cast<const half8 *>(sA + swz(wm * WTM + i * 32 + lr, 2 * s + lk));
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int g = lane >> 4, si = lane & 15;
+      const int row = 16 * s + 8 * (g >> 1) + (si >> 2);
+      const int col = wn * WTN + j * 32 + 16 * (g & 1) + 4 * (si & 3);
+      const int off = kn_off(row, col >> 3, KNP) + 8 * (si & 1);
+      const half4 lo = lds_read_tr16(sB + off), hi = lds_read_tr16(sB + off + 4 * KNP);
+      fb[slot][j] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  };
+  floatx16 acc[FM][FN];
+  for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j)
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+  // both stages start with operand slabs: the loops without fetches keep them
+  fetch(0, 0);
+  fetch(64, 1);
+  lds_dma_wait();
+  __syncthreads();
+  if constexpr (MODE == 0) {
+    read(smem, smem + kA, 0, 0);
+    read(smem, smem + kA, 1, 1);
+  }
+  half8 vr[32 / NW * 2], sink = {};
+  for (int kt = 0; kt < nslab; ++kt) {
+    const int buf = kt & 1, k1 = ((kt + 1) % (kK / 64)) * 64;
+    if constexpr (MODE == 2) fetch(k1, buf ^ 1);
+    if constexpr (MODE == 3) {
+      const int rsub = lane >> 3, pch = lane & 7, xsub = lane >> 5, xch = lane & 31;
+#pragma unroll
+      for (int i = 0; i < 32 / NW; ++i) {
+        const int row = (wave + i * NW) * 8 + rsub;
+        vr[i] = *reinterpret_cast<const half8 *>(A + size_t(m0 + row) * kK + k1 + pch * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < 32 / NW; ++i) {
+        const int row = (wave + i * NW) * 2 + xsub;
+        vr[32 / NW + i] = *reinterpret_cast<const half8 *>(X + size_t(k1 + row) * kLdx + n0 + xch * 8);
+      }
+    }
+    const char *sA = smem + buf * kStage, *sB = sA + kA;
+    if constexpr (MODE >= 1) read(sA, sB, 0, 0);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if constexpr (MODE >= 1)
+        if (s < 3) read(sA, sB, s + 1, (s + 1) & 1);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[s & 1][j], fa[s & 1][i], acc[i][j], 0, 0, 0);
+    }
+    if constexpr (MODE == 2) lds_dma_wait();
+    if constexpr (MODE == 3) {
+#pragma unroll
+      for (int i = 0; i < 32 / NW * 2; ++i) sink += vr[i];
+    }
+    __syncthreads();
+  }
+  float sum = float(sink[0]);
+  for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j)
+      for (int r = 0; r < 16; ++r) sum += acc[i][j][r];
+  if (tid == 0) {
+    clk[4 * blockIdx.x + 0] = clock64() - c0;
+    clk[4 * blockIdx.x + 1] = wall_clock64() - w0;
+    clk[4 * blockIdx.x + 2] = __builtin_bit_cast(unsigned, sum);   // keeps the MFMAs live
+  }
+}
+
+}  // namespace slorr
+
+using namespace slorr;
+
+int main() {
+  const int grid = 1280, nslab = 48, reps = 20;
+  _Float16 *A, *X;
+  unsigned long long *clk;
+  CK(hipMalloc(&A, size_t(kK) * kK * 2));
+  CK(hipMalloc(&X, size_t(kK) * kLdx * 2));
+  CK(hipMalloc(&clk, size_t(grid) * 4 * sizeof(unsigned long long)));
+  // uniform fp16 values in [-1, 1) from a 64-bit LCG (Knuth's MMIX constants)
+  std::vector<_Float16> ha(size_t(kK) * kK), hx(size_t(kK) * kLdx);
+  unsigned long long st = 12345;
+  auto uni = [&]() {
+    st = st * 6364136223846793005ULL + 1442695040888963407ULL;
+    return _Float16(float(st >> 40) * (2.0f / 16777216.0f) - 1.0f);
+  };
+  for (auto &v : ha) v = uni();
+  for (auto &v : hx) v = uni();
+  int wall_khz = 0;
+  CK(hipDeviceGetAttribute(&wall_khz, hipDeviceAttributeWallClockRate, 0));
+  hipEvent_t e0, e1;
+  CK(hipEventCreate(&e0));
+  CK(hipEventCreate(&e1));
+  std::vector<unsigned long long> h(size_t(grid) * 4);
+  typedef void (*kern_t)(unsigned long long *, const _Float16 *, const _Float16 *, int);
+  auto fill = [&](bool random) {
+    if (random) {
+      CK(hipMemcpy(A, ha.data(), ha.size() * 2, hipMemcpyHostToDevice));
+      CK(hipMemcpy(X, hx.data(), hx.size() * 2, hipMemcpyHostToDevice));
+    } else {
+      CK(hipMemset(A, 0, ha.size() * 2));
+      CK(hipMemset(X, 0, hx.size() * 2));
+    }
+  };
+  auto run = [&](const char *name, kern_t k, int nw) {
+    for (int r = 0; r < 3; ++r) hipLaunchKernelGGL(k, dim3(grid), dim3(nw * 64), 0, 0, clk, A, X, nslab);
+    CK(hipGetLastError());
+    CK(hipDeviceSynchronize());
+    CK(hipEventRecord(e0, 0));
+    for (int r = 0; r < reps; ++r) hipLaunchKernelGGL(k, dim3(grid), dim3(nw * 64), 0, 0, clk, A, X, nslab);
+    CK(hipEventRecord(e1, 0));
+    CK(hipEventSynchronize(e1));
+    float ms;
+    CK(hipEventElapsedTime(&ms, e0, e1));
+    CK(hipMemcpy(h.data(), clk, h.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    double cyc = 0, wall = 0;
+    for (int b = 0; b < grid; ++b) cyc += double(h[4 * b]), wall += double(h[4 * b + 1]);
+    const double ghz = cyc / wall * wall_khz * 1e-6;
+    const double us = ms * 1e3 / reps;
+    const double tf = double(grid) * 2.0 * 256 * 256 * 64 * nslab / (us * 1e-6) * 1e-12;
+    // 2.5 PF dense fp16 is 256 CUs x 4 SIMDs x 1024 flops per clock at 2.4 GHz
+    const double at_clock = 256.0 * 4 * 1024 * ghz * 1e-3;
+    printf("%-24s %d waves  %8.1f us  %7.1f TFLOP/s  clock %.2f GHz  (%3.0f%% of the MFMA rate at that clock)\n",
+           name, nw, us, tf, ghz, 100.0 * tf / at_clock);
+    fflush(stdout);
+  };
+  for (int random = 0; random < 2; ++random) {
+    fill(random);
+    printf("%s operands\n", random ? "random" : "zero");
+    run("MFMA only", k_ceiling<0, 8>, 8);
+    run("+ LDS fragment reads", k_ceiling<1, 8>, 8);
+    run("+ global->LDS fetches", k_ceiling<2, 8>, 8);
+    run("fetches to VGPRs", k_ceiling<3, 8>, 8);
+    run("MFMA only", k_ceiling<0, 4>, 4);
+    run("+ LDS fragment reads", k_ceiling<1, 4>, 4);
+    run("+ global->LDS fetches", k_ceiling<2, 4>, 4);
+  }
+  return 0;
+}
