@@ -251,6 +251,18 @@ __device__ __forceinline__ float as_stored(float v) {
   return v;
 }
 
+// The trace's partial over 8 consecutive columns of one row of an fp16 tile:
+// sum of P (as stored) times X_0', four v_dot2_f32_f16 in column order with
+// an fp32 running sum (each pair's products are formed exactly). The callers
+// add these partials in fp64.
+__device__ __forceinline__ float trace8(const half8 &p, const half8 &x0) {
+  float f = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 8; q += 2)
+    f = __builtin_amdgcn_fdot2(half2v{p[q], p[q + 1]}, half2v{x0[q], x0[q + 1]}, f, false);
+  return f;
+}
+
 template <typename T, typename Tw, int MODE, int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   using S = GemmShape<BM, BN, WGM, WGN>;
@@ -549,17 +561,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         }
         if (MODE == kUpdate || args.write_x) store8_stream(Xn + size_t(grow) * d.Qp + gcol, v);
         if (MODE == kLast) {
-          // P as stored times X_0' (both in the iterate's scale): the products
-          // of two fp16 (or fp32) values are exact in fp64
+          // P as stored times X_0' (both in the iterate's scale); fp32 sets:
+          // each product exact in fp64
+          if constexpr (MODE == kLast && sizeof(T) == 2) {
+            half8 ph;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            float x0;
-            if constexpr (APRE) {
-              x0 = apre[i & 1][t].get(j);
-            } else {
-              x0 = float(asrc[size_t(grow) * apitch + gcol + j]);
-            }
-            tsum += double(as_stored<T>(v[j])) * double(x0);
+            for (int j = 0; j < 8; ++j) ph[j] = _Float16(v[j]);
+            tsum += double(trace8(ph, apre[i & 1][t].h));
+          } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+              tsum += double(as_stored<T>(v[j])) * double(float(asrc[size_t(grow) * apitch + gcol + j]));
           }
         }
       }
@@ -955,12 +967,7 @@ __global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
         const half8 h = *reinterpret_cast<const half8 *>(ep + epi_off(row, ch));
         const size_t o = size_t(row_w + i * 32 + row) * cur.ldx + col_w + 8 * ch;
         if (MODE == kUpdate || args.write_x) __builtin_nontemporal_store(h, reinterpret_cast<half8 *>(cur.Xn + o));
-        if constexpr (MODE == kLast) {
-          // P as stored times X_0' (both in the iterate's scale): the
-          // products of two fp16 values are exact in fp64
-#pragma unroll
-          for (int q = 0; q < 8; ++q) tsum += double(h[q]) * double(x0v[i & 1][t][q]);
-        }
+        if constexpr (MODE == kLast) tsum += double(trace8(h, x0v[i & 1][t]));   // P as stored times X_0'
       }
       if (i + 2 < U::FM) x0load(cur, i + 2);
       __builtin_amdgcn_wave_barrier();
