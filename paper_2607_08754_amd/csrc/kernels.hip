@@ -153,6 +153,64 @@ __device__ __forceinline__ void put8(T *p, int n, const float (&v)[8]) {
   }
 }
 
+// The full-tile path of the tile kernels below: 16-byte accesses known to be
+// aligned and in bounds, issued as global-memory instructions with no branch
+// between them, so that all of a thread's loads are in flight together (the
+// weight and gradient pointers come from a device table: left to itself the
+// compiler cannot tell their address space and emits flat accesses).
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 gload16(const void *p) {
+  return *(const __attribute__((address_space(1))) u32x4 *)p;
+}
+__device__ __forceinline__ void gstore16(void *p, u32x4 v) { *(__attribute__((address_space(1))) u32x4 *)p = v; }
+
+// 8 consecutive values, 16-byte aligned and all in bounds, as floats.
+template <typename T>
+__device__ __forceinline__ void ld8(const T *p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    typedef T t8 __attribute__((ext_vector_type(8)));
+    const t8 h = __builtin_bit_cast(t8, gload16(p));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = to_f(T(h[j]));
+  } else {
+    const float4v a = __builtin_bit_cast(float4v, gload16(p)), b = __builtin_bit_cast(float4v, gload16(p + 4));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = a[j];
+      v[4 + j] = b[j];
+    }
+  }
+}
+
+// 8 consecutive values to p, 16-byte aligned and all in bounds (the rounding
+// of put8).
+template <typename T>
+__device__ __forceinline__ void st8(T *p, const float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    typedef T t8 __attribute__((ext_vector_type(8)));
+    t8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = from_f<T>(v[j]);
+    gstore16(p, __builtin_bit_cast(u32x4, h));
+  } else {
+    float4v a, b;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      a[j] = v[j];
+      b[j] = v[4 + j];
+    }
+    gstore16(p, __builtin_bit_cast(u32x4, a));
+    gstore16(p + 4, __builtin_bit_cast(u32x4, b));
+  }
+}
+
+// Whether canonical tile t lies inside the matrix and the rows of W (of
+// element size es) start 16-byte aligned: then every access of the tile to W
+// is an aligned 16-byte run (the base pointers are 16-byte aligned).
+__device__ __forceinline__ bool full_tile(const Tile &t, const MatDesc &d, size_t es) {
+  return (t.tm + 1) * kPrepTile <= d.P && (t.tn + 1) * kPrepTile <= d.Q && (size_t(d.cols) * es) % 16 == 0;
+}
+
 // --------------------------------------------------------------- reductions
 
 // 64 x 64 canonical tile per block (the tiles of the normalisation), staged in
@@ -167,11 +225,7 @@ __device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const Mat
   // source rows of W covered by the tile: wide -> canonical rows m, tall -> canonical columns n
   const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;
   const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
-  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
-    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
-    float v[8];
-    const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
-    get8(w + size_t(r0 + r) * d.cols + c0 + c, nv, v);
+  auto put = [&](int r, int c, const float (&v)[8]) {
     if (d.tall) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) tile[(c + j) * kPrepPitch + r] = v[j] * scale;
@@ -179,6 +233,29 @@ __device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const Mat
 #pragma unroll
       for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j] * scale;
     }
+  };
+  constexpr int kTasks = kPrepTile * kPrepTile / 8 / kThreads;
+  static_assert(kTasks * kThreads * 8 == kPrepTile * kPrepTile, "tile task split");
+  if (full_tile(t, d, sizeof(Tw))) {
+    float v[kTasks][8];
+#pragma unroll
+    for (int k = 0; k < kTasks; ++k) {
+      const int q = threadIdx.x + k * kThreads, r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+      ld8(w + size_t(r0 + r) * d.cols + c0 + c, v[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < kTasks; ++k) {
+      const int q = threadIdx.x + k * kThreads;
+      put(q / (kPrepTile / 8), (q % (kPrepTile / 8)) * 8, v[k]);
+    }
+    return;
+  }
+  for (int q = threadIdx.x; q < kPrepTile * kPrepTile / 8; q += kThreads) {
+    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+    float v[8];
+    const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
+    get8(w + size_t(r0 + r) * d.cols + c0 + c, nv, v);
+    put(r, c, v);
   }
 }
 
@@ -206,10 +283,15 @@ __global__ __launch_bounds__(kThreads) void k_sumsq(const Tile *__restrict__ til
   // W it reads start at r0 (wide: canonical rows, tall: canonical columns)
   const int cm = t.tm * kPrepTile + 8 * (lane >> 3), cn = t.tn * kPrepTile + 8 * (lane & 7);
   const int r0 = d.tall ? cn : cm, c0 = d.tall ? cm : cn;
-  const int nv = max(0, min(8, d.cols - c0));
   float v[8][8];
+  if (full_tile(t, d, sizeof(Tw))) {
 #pragma unroll
-  for (int a = 0; a < 8; ++a) get8(w + size_t(r0 + a) * d.cols + c0, r0 + a < d.rows ? nv : 0, v[a]);
+    for (int a = 0; a < 8; ++a) ld8(w + size_t(r0 + a) * d.cols + c0, v[a]);
+  } else {
+    const int nv = max(0, min(8, d.cols - c0));
+#pragma unroll
+    for (int a = 0; a < 8; ++a) get8(w + size_t(r0 + a) * d.cols + c0, r0 + a < d.rows ? nv : 0, v[a]);
+  }
   double acc = 0.0;
   if (!d.tall) {
 #pragma unroll
@@ -292,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(const Tile *__restrict__ tile
     float v[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) v[j] = tile[r * kPrepPitch + c + j];
-    put8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
+    st8(x + size_t(m0 + r) * d.Qp + n0 + c, v);   // padded canonical buffer: aligned, in bounds
   }
 }
 
@@ -459,22 +541,34 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   constexpr int kTasks = kPrepTile * kPrepTile / 8 / kThreads;
   const int r0 = d.tall ? n0 : m0, c0 = d.tall ? m0 : n0;     // rows / columns of W
   const int rlim = d.tall ? d.Q : d.P, clim = d.tall ? d.P : d.Q;
+  const bool full = full_tile(t, d, sizeof(Tw)) && (size_t(d.cols) * sizeof(Tg)) % 16 == 0;
   float wv[kTasks][8], old[kTasks][8];
+  if (full) {
 #pragma unroll
-  for (int k = 0; k < kTasks; ++k) {
-    const int q = threadIdx.x + k * kThreads;
-    const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
-    const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
-    const size_t o = size_t(r0 + r) * d.cols + c0 + c;
-    get8(w + o, nv, wv[k]);
-    if (accumulate) get8(g + o, nv, old[k]);
+    for (int k = 0; k < kTasks; ++k) {
+      const int q = threadIdx.x + k * kThreads;
+      const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+      const size_t o = size_t(r0 + r) * d.cols + c0 + c;
+      ld8(w + o, wv[k]);
+      if (accumulate) ld8(g + o, old[k]);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kTasks; ++k) {
+      const int q = threadIdx.x + k * kThreads;
+      const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
+      const int nv = (r0 + r < rlim) ? max(0, min(8, clim - (c0 + c))) : 0;
+      const size_t o = size_t(r0 + r) * d.cols + c0 + c;
+      get8(w + o, nv, wv[k]);
+      if (accumulate) get8(g + o, nv, old[k]);
+    }
   }
 #pragma unroll
   for (int k = 0; k < kTasks; ++k) {
     const int q = threadIdx.x + k * kThreads;
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
     float v[8];
-    get8(x + size_t(m0 + r) * d.Qp + n0 + c, 8, v);
+    ld8(x + size_t(m0 + r) * d.Qp + n0 + c, v);     // padded canonical buffer: aligned, in bounds
 #pragma unroll
     for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j];
   }
@@ -483,7 +577,7 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
   for (int k = 0; k < kTasks; ++k) {
     const int q = threadIdx.x + k * kThreads;
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
-    if (r0 + r >= rlim || c0 + c >= clim) continue;
+    if (!full && (r0 + r >= rlim || c0 + c >= clim)) continue;
     const int nv = min(8, clim - (c0 + c));
     const size_t o = size_t(r0 + r) * d.cols + c0 + c;
     float v[8];
@@ -498,7 +592,10 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = old[k][j] + v[j];
     }
-    put8(g + o, nv, v);
+    if (full)
+      st8(g + o, v);
+    else
+      put8(g + o, nv, v);
   }
 }
 

@@ -303,8 +303,11 @@ void build_plan(Plan &p) {
   }
   p.trace_slots = slot;
   // canonical 64 x 64 tiles: the norm (one partial slot each, contiguous per
-  // matrix, summed in tile order), the normalisation and the gradient; element
-  // runs of the original layout for the decoupled update
+  // matrix in canonical row-major tile order, which is the order they are
+  // summed in), the normalisation and the gradient; element runs of the
+  // original layout for the decoupled update. The list walks each matrix along
+  // W's own rows (tall W: down the canonical columns), so that the 4 waves of
+  // a block read adjacent 128-byte pieces of the same rows of W.
   p.chunks.clear();
   p.prep.first = int32_t(p.tiles.size());
   int32_t nslot = 0;
@@ -312,8 +315,15 @@ void build_plan(Plan &p) {
     MatDesc &d = p.mats[i];
     if (d.empty) continue;
     d.norm_begin = nslot;
-    for (int tm = 0; tm < d.Pp / kPrepTile; ++tm)
-      for (int tn = 0; tn < d.Qp / kPrepTile; ++tn) p.tiles.push_back(make_tile(i, tm, tn, nslot++));
+    const int ntm = d.Pp / kPrepTile, ntn = d.Qp / kPrepTile;
+    if (d.tall) {
+      for (int tn = 0; tn < ntn; ++tn)
+        for (int tm = 0; tm < ntm; ++tm) p.tiles.push_back(make_tile(i, tm, tn, nslot + tm * ntn + tn));
+    } else {
+      for (int tm = 0; tm < ntm; ++tm)
+        for (int tn = 0; tn < ntn; ++tn) p.tiles.push_back(make_tile(i, tm, tn, nslot + tm * ntn + tn));
+    }
+    nslot += ntm * ntn;
     d.norm_end = nslot;
     const int64_t total = int64_t(d.rows) * d.cols;
     for (int64_t b = 0; b < total; b += kChunk)
