@@ -283,7 +283,9 @@ void build_plan(Plan &p) {
     bool all_big = !order.empty() && f16;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
-      all_big &= d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0;
+      // the 256-tile update addresses each operand matrix through a buffer
+      // resource with 32-bit byte offsets: matrices under 2 GiB
+      all_big &= d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0 && int64_t(d.Pp) * d.Qp * 2 < (int64_t(1) << 31);
       big += int64_t(d.Pp / kBigTile) * (d.Qp / kBigTile);
     }
     const int cfg = (all_big && big >= kMinBigTiles) ? kCfg256 : kCfg128;
