@@ -76,8 +76,10 @@ typedef enum { SLORR_F32 = 0, SLORR_BF16 = 1 } slorr_dtype_t;
 
 /* Shape of one weight matrix: row-major, contiguous, rows x cols.
  * A conv kernel (C_out, C_in, k_h, k_w) is passed as (C_out, C_in*k_h*k_w)
- * (App. C.1). rows, cols >= 0; min(rows, cols) <= 16384 and
- * max(rows, cols) <= 1048576 (SLORR_ERR_UNSUPPORTED otherwise). A matrix with
+ * (App. C.1). rows, cols >= 0; min(rows, cols) <= 16384,
+ * max(rows, cols) <= 1048576, and the matrix with both dimensions rounded up
+ * to multiples of 128 under 2 GiB in the iterate type (2 bytes per element
+ * for SLORR_BF16, 4 for SLORR_F32); SLORR_ERR_UNSUPPORTED otherwise. A matrix with
  * rows == 0 or cols == 0 has value 0 and no gradient elements. */
 typedef struct { int32_t rows, cols; } slorr_shape_t;
 

@@ -102,30 +102,19 @@ struct GemmShape {
 __device__ __forceinline__ int swz_key(int row) { return (row & 7) ^ ((row >> 3) & 1); }
 __device__ __forceinline__ int swz(int row, int chunk) { return row * 128 + ((chunk ^ swz_key(row)) << 4); }
 
-// 16 bytes per lane from global memory straight into LDS: lane l's bytes land
-// at lds_base + 16 l (lds_base wave-uniform, passed in m0). Device pass only:
-// the host pass of the single-source build just needs the kernel's stub.
+// 16 bytes per lane from a buffer straight into LDS: byte voff + soff of the
+// buffer (voff per lane, soff wave-uniform) lands at lds_base + 16 l
+// (lds_base wave-uniform, passed in m0). On the update tile's k loop this
+// form issues at a markedly lower cost than global_load_lds_dwordx4 with a
+// 64-bit address per lane; a load past the buffer's size returns zeros
+// instead of faulting. Device pass only: the host pass of the single-source
+// build just needs the kernel's stub.
 //
 // Issued through inline assembly: the compiler then does not track these LDS
 // writes and puts no wait for them before later LDS reads (it cannot tell
-// that those read the other stage). Completion is the caller's job: the
-// block barrier at the end of each k-slab waits for every outstanding load.
-__device__ __forceinline__ void load_lds16(const void *g, void *lds_base) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  // the low 32 bits of a flat address into LDS are the LDS byte address
-  const uint32_t m = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(lds_base)));
-  asm volatile("global_load_lds_dwordx4 %1, off" : : "{m0}"(m), "v"(g) : "memory");
-#else
-  (void)g;
-  (void)lds_base;
-#endif
-}
-
-// The same global -> LDS load through a buffer resource: 16 bytes per lane
-// from byte voff + soff of the buffer (voff per lane, soff wave-uniform) to
-// lds_base + 16 l. Measured on the update tile's k loop it issues at a
-// markedly lower cost than the 64-bit-address form above; a load past the
-// buffer's size returns zeros instead of faulting.
+// that those read the other stage). Completion is the caller's job: each
+// k-slab is waited for by count (s_waitcnt vmcnt) before the block barrier
+// that publishes it.
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ i32x4 buffer_rsrc(const void *base, uint32_t bytes) {
   const uint64_t b = uint64_t(uintptr_t(base));
@@ -175,7 +164,7 @@ __device__ __forceinline__ int kn_off(int row, int chunk, int pitch) {
 }
 
 // Wait until every global -> LDS load this wave issued has landed (the
-// compiler does not count them, see load_lds16); precedes the block barrier
+// compiler does not count them, see buffer_load_lds16); precedes the block barrier
 // that publishes a stage.
 __device__ __forceinline__ void lds_dma_wait() {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -348,39 +337,56 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const int lr = lane & 31, lk = lane >> 5;
   const int wm = wave / WGN, wn = wave % WGN;
 
-  // Direct global -> LDS loads (global_load_lds_dwordx4) of the K-major
+  // Direct global -> LDS loads (buffer_load_dwordx4 ... lds) of the K-major
   // operands: one wave instruction fills 8 consecutive LDS rows (1 KB) at the
   // wave-uniform base in m0, lane l landing at base + 16 l, i.e. row l / 8,
   // physical chunk l % 8; the lane therefore fetches logical chunk
-  // (l % 8) ^ key(row). No registers, no ds_write instructions.
+  // (l % 8) ^ key(row). No registers, no ds_write instructions. Each operand
+  // matrix is one buffer resource (under 2 GiB, the plan's limit); a lane's
+  // byte offset is fixed for the tile, and the slab and the instruction's row
+  // step (a multiple of the swizzle key's period) go into the scalar offset.
+  const T *Abase = Ap, *Bbase = Bp;               // the operand matrices (Gram parts: from k0)
+  const uint32_t abytes = uint32_t(d.Pp) * uint32_t(lda) * sizeof(T) - uint32_t(part ? tile.k0 : 0) * sizeof(T);
+  const uint32_t bbytes = uint32_t(d.Pp) * uint32_t(ldb) * sizeof(T) - uint32_t(part ? tile.k0 : 0) * sizeof(T);
+  static_assert((8 * S::kWaves) % 16 == 0, "swizzle period");
   auto dload = [&](int k0, int buf) {
     char *sA = smem + buf * S::kStage;
     char *sB = sA + BM * 128;
     const int rsub = lane >> 3, pch = lane & 7;
+    constexpr uint32_t kRowStep = 8 * S::kWaves;  // rows between a wave's instructions
+    {
+      const i32x4 ra = buffer_rsrc(Abase, abytes);
+      const int row = wave * 8 + rsub;
+      const uint32_t voff = (uint32_t(m0 + row) * uint32_t(lda) + uint32_t((pch ^ swz_key(row)) * V)) * sizeof(T);
 #pragma unroll
-    for (int i = 0; i < BM / 8 / S::kWaves; ++i) {
-      const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
-      load_lds16(Ap + size_t(m0 + row) * lda + k0 + (pch ^ swz_key(row)) * V, sA + r0 * 128);
+      for (int i = 0; i < BM / 8 / S::kWaves; ++i)
+        buffer_load_lds16(ra, voff, (uint32_t(k0) + uint32_t(i) * kRowStep * uint32_t(lda)) * sizeof(T),
+                          sA + (wave + i * S::kWaves) * 8 * 128);
     }
     if constexpr (TR) {
       // one wave instruction fills 1024 / KNP consecutive k-rows; lane l lands
       // at physical chunk l % (KNP / 16) of its row and fetches the logical
       // chunk that kn_off puts there
       constexpr int CPR = KNP / 16, RPI = 1024 / KNP;
-      const int rsub = lane / CPR, pch = lane % CPR;
+      static_assert((RPI * S::kWaves) % 4 == 0, "kn_off key period");
+      const int xsub = lane / CPR, xch = lane % CPR;
+      const i32x4 rb = buffer_rsrc(Bbase, bbytes);
+      const int row = wave * RPI + xsub;
+      const uint32_t voff = (uint32_t(row) * uint32_t(ldb) + uint32_t(n0 + (xch ^ ((row & 3) << 2)) * V)) * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < BK / RPI / S::kWaves; ++i) {
-        const int r0 = (wave + i * S::kWaves) * RPI, row = r0 + rsub;
-        load_lds16(Bp + size_t(k0 + row) * ldb + n0 + (pch ^ ((row & 3) << 2)) * V, sB + r0 * KNP);
-      }
+      for (int i = 0; i < BK / RPI / S::kWaves; ++i)
+        buffer_load_lds16(rb, voff, (uint32_t(k0) + uint32_t(i * RPI * S::kWaves)) * uint32_t(ldb) * sizeof(T),
+                          sB + (wave + i * S::kWaves) * RPI * KNP);
     }
     if constexpr (!KN) {
       if (diag) return;                 // both operands are the same rows: one copy
+      const i32x4 rb = buffer_rsrc(Bbase, bbytes);
+      const int row = wave * 8 + rsub;
+      const uint32_t voff = (uint32_t(n0 + row) * uint32_t(ldb) + uint32_t((pch ^ swz_key(row)) * V)) * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < BN / 8 / S::kWaves; ++i) {
-        const int r0 = (wave + i * S::kWaves) * 8, row = r0 + rsub;
-        load_lds16(Bp + size_t(n0 + row) * ldb + k0 + (pch ^ swz_key(row)) * V, sB + r0 * 128);
-      }
+      for (int i = 0; i < BN / 8 / S::kWaves; ++i)
+        buffer_load_lds16(rb, voff, (uint32_t(k0) + uint32_t(i) * kRowStep * uint32_t(ldb)) * sizeof(T),
+                          sB + (wave + i * S::kWaves) * 8 * 128);
     }
   };
   // the transposing loader of the [k][n] operand (update) into registers

@@ -16,6 +16,9 @@ namespace {
 constexpr int64_t kMaxShort = 16384;
 constexpr int64_t kMaxLong = 1 << 20;
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+// the GEMM kernels address each operand matrix (padded canonical shape, in
+// the iterate type) through a buffer resource with 32-bit byte offsets
+constexpr int64_t kMaxIterBytes = int64_t(1) << 31;
 constexpr int64_t kMinBigTiles = 2 * kCus;  // two 256-tiles per CU
 constexpr int64_t kMinGramUnits = 2 * kCus; // Gram blocks wanted per launch (two per CU)
 constexpr int kMaxGramParts = 16;           // k parts per Gram tile at most
@@ -107,6 +110,8 @@ void build_plan(Plan &p) {
     d.Qp = round_up(d.Q, kTile);
     if (r * c > kMaxElems || int64_t(d.Pp) * d.Qp > kMaxElems)
       throw std::domain_error("matrix has more than 2^31 - 1 elements");
+    if (int64_t(d.Pp) * d.Qp * int64_t(p.iter_bytes()) >= kMaxIterBytes)
+      throw std::domain_error("matrix of 2 GiB or more in the iterate type (padded canonical shape)");
     groups[{d.P, d.Q}]++;
     p.paper_flops += p.iters * (4.0 * P * P * Q + 2.0 * P * P * P);
     p.weight_bytes += double(r) * c * p.elem_bytes();
@@ -283,9 +288,7 @@ void build_plan(Plan &p) {
     bool all_big = !order.empty() && f16;
     for (int i : order) {
       const MatDesc &d = p.mats[i];
-      // the 256-tile update addresses each operand matrix through a buffer
-      // resource with 32-bit byte offsets: matrices under 2 GiB
-      all_big &= d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0 && int64_t(d.Pp) * d.Qp * 2 < (int64_t(1) << 31);
+      all_big &= d.Pp % kBigTile == 0 && d.Qp % kBigTile == 0;
       big += int64_t(d.Pp / kBigTile) * (d.Qp / kBigTile);
     }
     const int cfg = (all_big && big >= kMinBigTiles) ? kCfg256 : kCfg128;

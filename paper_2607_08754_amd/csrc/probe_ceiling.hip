@@ -6,7 +6,11 @@
 //   MFMA only         fragments read once, then only MFMAs and the barrier
 //   + LDS reads       the fragment reads of each k step (row operand by
 //                     16-byte reads, [k][n] operand by ds_read_b64_tr_b16)
-//   + fetches         the next slab's operands fetched global -> LDS
+//   + fetches         the next slab's operands fetched global -> LDS with
+//                     global_load_lds_dwordx4 (a 64-bit address per lane)
+//   + buffer fetches  the same fetches with buffer_load_dwordx4 ... lds (a
+//                     buffer resource per operand, a 32-bit offset per lane:
+//                     the form the library's kernels use)
 //   fetches to VGPRs  as "+ fetches", but the same bytes are loaded into
 //                     registers and discarded: no LDS write at all
 //
@@ -37,10 +41,24 @@
 
 namespace slorr {
 
+// 16 bytes per lane from global memory straight into LDS (lane l at
+// lds_base + 16 l, lds_base in m0), addressed by a 64-bit pointer per lane.
+__device__ __forceinline__ void load_lds16(const void *g, void *lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // the low 32 bits of a flat address into LDS are the LDS byte address
+  const uint32_t m = __builtin_amdgcn_readfirstlane(uint32_t(uintptr_t(lds_base)));
+  asm volatile("global_load_lds_dwordx4 %1, off" : : "{m0}"(m), "v"(g) : "memory");
+#else
+  (void)g;
+  (void)lds_base;
+#endif
+}
+
 constexpr int kK = 768, kLdx = 3072;   // operand extents: A is kK x kK, X is kK x kLdx
 
 // MODE 0: MFMA only; 1: + LDS fragment reads; 2: + global -> LDS fetches;
-// 3: MODE 1 + the fetches' loads into registers (no LDS write).
+// 3: MODE 1 + the fetches' loads into registers (no LDS write); 4: MODE 1 +
+// the fetches through buffer resources.
 template <int MODE, int NW>
 __global__ __launch_bounds__(NW * 64) void k_ceiling(unsigned long long *clk, const _Float16 *A,
                                                      const _Float16 *X, int nslab) {
@@ -65,6 +83,23 @@ __global__ __launch_bounds__(NW * 64) void k_ceiling(unsigned long long *clk, co
     for (int i = 0; i < 32 / NW; ++i) {   // 64 rows of 512 bytes, 2 rows per instruction
       const int r0 = (wave + i * NW) * 2, row = r0 + xsub;
       load_lds16(X + size_t(k0 + row) * kLdx + n0 + (xch ^ ((row & 3) << 2)) * 8, sB + r0 * KNP);
+    }
+  };
+  const i32x4 ra = buffer_rsrc(A, uint32_t(kK) * kK * 2), rx = buffer_rsrc(X, uint32_t(kK) * kLdx * 2);
+  auto bfetch = [&](int k0, int buf) {
+    char *sA = smem + buf * kStage, *sB = sA + kA;
+    const int rsub = lane >> 3, pch = lane & 7;
+#pragma unroll
+    for (int i = 0; i < 32 / NW; ++i) {
+      const int r0 = (wave + i * NW) * 8, row = r0 + rsub;
+      buffer_load_lds16(ra, uint32_t((m0 + row) * kK + (pch ^ swz_key(row)) * 8) * 2, uint32_t(k0) * 2, sA + r0 * 128);
+    }
+    const int xsub = lane >> 5, xch = lane & 31;
+#pragma unroll
+    for (int i = 0; i < 32 / NW; ++i) {
+      const int r0 = (wave + i * NW) * 2, row = r0 + xsub;
+      buffer_load_lds16(rx, uint32_t(row * kLdx + n0 + (xch ^ ((row & 3) << 2)) * 8) * 2, uint32_t(k0 * kLdx) * 2,
+                        sB + r0 * KNP);
     }
   };
   half8 fa[2][FM], fb[2][FN];
@@ -99,6 +134,7 @@ __global__ __launch_bounds__(NW * 64) void k_ceiling(unsigned long long *clk, co
   for (int kt = 0; kt < nslab; ++kt) {
     const int buf = kt & 1, k1 = ((kt + 1) % (kK / 64)) * 64;
     if constexpr (MODE == 2) fetch(k1, buf ^ 1);
+    if constexpr (MODE == 4) bfetch(k1, buf ^ 1);
     if constexpr (MODE == 3) {
       const int rsub = lane >> 3, pch = lane & 7, xsub = lane >> 5, xch = lane & 31;
 #pragma unroll
@@ -124,7 +160,7 @@ __global__ __launch_bounds__(NW * 64) void k_ceiling(unsigned long long *clk, co
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[s & 1][j], fa[s & 1][i], acc[i][j], 0, 0, 0);
     }
-    if constexpr (MODE == 2) lds_dma_wait();
+    if constexpr (MODE == 2 || MODE == 4) lds_dma_wait();
     if constexpr (MODE == 3) {
 #pragma unroll
       for (int i = 0; i < 32 / NW * 2; ++i) sink += vr[i];
@@ -206,10 +242,12 @@ int main() {
     run("MFMA only", k_ceiling<0, 8>, 8);
     run("+ LDS fragment reads", k_ceiling<1, 8>, 8);
     run("+ global->LDS fetches", k_ceiling<2, 8>, 8);
+    run("+ buffer->LDS fetches", k_ceiling<4, 8>, 8);
     run("fetches to VGPRs", k_ceiling<3, 8>, 8);
     run("MFMA only", k_ceiling<0, 4>, 4);
     run("+ LDS fragment reads", k_ceiling<1, 4>, 4);
     run("+ global->LDS fetches", k_ceiling<2, 4>, 4);
+    run("+ buffer->LDS fetches", k_ceiling<4, 4>, 4);
   }
   return 0;
 }

@@ -193,6 +193,16 @@ def test_plan_errors(L):
                        (4, (1 << 20) + 1, L.ERR_UNSUPPORTED), (16384, 1 << 20, L.ERR_UNSUPPORTED)]:
         st, _, _, _ = _plan(L, [(r, c)])
         assert st == want, (r, c, st)
+    # the padded canonical matrix must stay under 2 GiB in the iterate type
+    # (fp32 sets: 4 bytes, bf16 sets: 2 bytes per element)
+    for r, c, dt, want in [(16384, 32768, 0, L.ERR_UNSUPPORTED), (16300, 32700, 0, L.ERR_UNSUPPORTED),
+                           (32640, 16384, 0, L.OK), (16384, 65536, 1, L.ERR_UNSUPPORTED), (16384, 65408, 1, L.OK)]:
+        st, h, _, _ = _plan(L, [(r, c)], dtype=dt)
+        assert st == want, (r, c, dt, st)
+        if st == L.OK:
+            assert lib.slorr_plan_destroy(h) == L.OK
+        else:
+            assert b"2 GiB" in lib.slorr_last_error()
     # dtype / kind
     assert _plan(L, [(4, 8)], dtype=7)[0] == L.ERR_UNSUPPORTED
     assert _plan(L, [(4, 8)], kind=9)[0] == L.ERR_UNSUPPORTED
