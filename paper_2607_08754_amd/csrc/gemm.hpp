@@ -348,20 +348,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const T *Abase = Ap, *Bbase = Bp;               // the operand matrices (Gram parts: from k0)
   const uint32_t abytes = uint32_t(d.Pp) * uint32_t(lda) * sizeof(T) - uint32_t(part ? tile.k0 : 0) * sizeof(T);
   const uint32_t bbytes = uint32_t(d.Pp) * uint32_t(ldb) * sizeof(T) - uint32_t(part ? tile.k0 : 0) * sizeof(T);
-  static_assert((8 * S::kWaves) % 16 == 0, "swizzle period");
+  // With 8 waves (two per SIMD) and two K-major operands (Gram, poly), only
+  // the first 4 waves fetch, one per SIMD: the other wave of the SIMD keeps
+  // the MFMA pipe busy while the fetching one waits to issue.
+  constexpr int kFW = (S::kWaves == 8 && !KN) ? 4 : S::kWaves;
+  constexpr uint32_t kRowStep = 8 * kFW;          // rows between a wave's instructions
+  static_assert(kRowStep % 16 == 0 && BM % kRowStep == 0 && BN % kRowStep == 0, "swizzle period");
   auto dload = [&](int k0, int buf) {
     char *sA = smem + buf * S::kStage;
     char *sB = sA + BM * 128;
     const int rsub = lane >> 3, pch = lane & 7;
-    constexpr uint32_t kRowStep = 8 * S::kWaves;  // rows between a wave's instructions
+    if (wave >= kFW) return;
     {
       const i32x4 ra = buffer_rsrc(Abase, abytes);
       const int row = wave * 8 + rsub;
       const uint32_t voff = (uint32_t(m0 + row) * uint32_t(lda) + uint32_t((pch ^ swz_key(row)) * V)) * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < BM / 8 / S::kWaves; ++i)
+      for (int i = 0; i < BM / 8 / kFW; ++i)
         buffer_load_lds16(ra, voff, (uint32_t(k0) + uint32_t(i) * kRowStep * uint32_t(lda)) * sizeof(T),
-                          sA + (wave + i * S::kWaves) * 8 * 128);
+                          sA + (wave + i * kFW) * 8 * 128);
     }
     if constexpr (TR) {
       // one wave instruction fills 1024 / KNP consecutive k-rows; lane l lands
@@ -384,9 +389,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
       const int row = wave * 8 + rsub;
       const uint32_t voff = (uint32_t(n0 + row) * uint32_t(ldb) + uint32_t((pch ^ swz_key(row)) * V)) * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < BN / 8 / S::kWaves; ++i)
+      for (int i = 0; i < BN / 8 / kFW; ++i)
         buffer_load_lds16(rb, voff, (uint32_t(k0) + uint32_t(i) * kRowStep * uint32_t(ldb)) * sizeof(T),
-                          sB + (wave + i * S::kWaves) * 8 * 128);
+                          sB + (wave + i * kFW) * 8 * 128);
     }
   };
   // the transposing loader of the [k][n] operand (update) into registers
