@@ -909,6 +909,19 @@ __global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
         for (int j = 0; j < U::FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fb[s & 1][j], fa[s & 1][i], acc[i][j], 0, 0, 0);
     }
+    // instruction order: the first k-step's fragment reads, then each MFMA
+    // followed by one read of the next k-step (8 of each per step), so the
+    // reads land under the MFMAs instead of bunching at the step's start
+    constexpr int kReads = U::FM + 2 * U::FN, kMfma = U::FM * U::FN;
+    static_assert(kReads == kMfma, "one read per MFMA");
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);      // LDS reads
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s)
+#pragma unroll
+      for (int q = 0; q < kMfma; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // MFMA
+        if (s + 1 < BK / 16) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
   };
 
   load_table(0);
