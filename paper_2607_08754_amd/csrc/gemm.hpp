@@ -90,7 +90,9 @@ struct GemmShape {
   static constexpr int kStage = (BM + BN) * 128;         // bytes per LDS stage
   static constexpr int kEpiPitch = WTN + 4;              // floats per staged row
   static constexpr int kEpiWave = 32 * kEpiPitch * 4;    // staged bytes per wave
-  static constexpr int kSmem = (2 * kStage > kWaves * kEpiWave) ? 2 * kStage : kWaves * kEpiWave;
+  static constexpr int kEpiHalf = 32 * WTN * 2;          // per wave: the fp16 block a mirror transposes
+  static constexpr int kEpiAll = kWaves * (kEpiWave + kEpiHalf);
+  static constexpr int kSmem = (2 * kStage > kEpiAll) ? 2 * kStage : kEpiAll;
 };
 
 // Byte offset of 16-byte chunk `chunk` of LDS row `row`. The XOR key
@@ -258,6 +260,26 @@ __device__ __forceinline__ void store8_range(T *p, const float (&v)[8], int lo, 
 #pragma unroll
   for (int j = 0; j < 8; ++j)
     if (j >= lo && j < hi) p[j] = T(v[j]);
+}
+
+// Byte offset of 16-byte chunk `chunk` (0..7) of row `row` (0..31) of a
+// wave's fp16 mirror block (32 rows of 64 values). The key spreads the rows
+// that one transposing read touches (4 consecutive rows in each of four
+// 8-row groups, 2 chunks each) over all 64 banks at two accesses per bank.
+__device__ __forceinline__ int mir_off(int row, int chunk) {
+  const int key = (((row >> 3) & 3) << 1) | ((row >> 1) & 1);
+  return row * 128 + ((chunk ^ key) << 4);
+}
+
+// 8 fp16 values to p[lo .. hi) (all 8 with one 16-byte store when whole).
+__device__ __forceinline__ void store_h8_range(_Float16 *p, const half8 &h, int lo, int hi) {
+  if (lo <= 0 && hi >= 8) {
+    *reinterpret_cast<half8 *>(p) = h;
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if (j >= lo && j < hi) p[j] = h[j];
 }
 
 // The value the iterate buffer holds for an fp32 result v (the rounding of
@@ -503,6 +525,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   constexpr int P = S::kEpiPitch;
   constexpr int CG = WTN / 8;                     // 8-column groups per staged row
   float *ep = reinterpret_cast<float *>(smem + wave * S::kEpiWave);
+  // fp16 sets: the mirror's block in fp16, transposed by ds_read_b64_tr_b16
+  constexpr bool kHalfMirror = sizeof(T) == 2 && WTN == 64;
+  char *eh = smem + S::kWaves * S::kEpiWave + wave * S::kEpiHalf;
   // per-matrix coefficients of the first step (kappa = 2^e / (f + eps))
   float alpha = args.alpha, beta = args.beta, gamma = args.gamma;
   if (args.kap) {
@@ -615,18 +640,44 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
         }
       }
       if (mirror) {
-        float4v e0, e1;
+        if constexpr (kHalfMirror) {
+          half8 hv;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          e0[j] = v[j];
-          e1[j] = v[4 + j];
+          for (int j = 0; j < 8; ++j) hv[j] = _Float16(v[j]);
+          *reinterpret_cast<half8 *>(eh + mir_off(row, cg)) = hv;
+        } else {
+          float4v e0, e1;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            e0[j] = v[j];
+            e1[j] = v[4 + j];
+          }
+          e[0] = e0;
+          e[1] = e1;
         }
-        e[0] = e0;
-        e[1] = e1;
       }
     }
     __builtin_amdgcn_wave_barrier();
-    if (mirror) {
+    if (mirror && kHalfMirror) {
+      // transpose: each 16-lane group takes 16 columns x 8 rows; two
+      // transposing reads (rows 0-3, 4-7 of the group) leave lane s with
+      // column 16 cb + s, rows 8 rg .. 8 rg + 7: one 16-byte row piece of
+      // the mirror tile
+#pragma unroll
+      for (int t = 0; t < NTASK; ++t) {
+        const int q = (lane >> 4) + 4 * t, rg = q & 3, cb = q >> 2, si = lane & 15;
+        const int col = 16 * cb + 4 * (si & 3);            // this lane's 4-column piece
+        const int r = 8 * rg + (si >> 2);
+        const int off = (col & 7) * 2;                     // byte within the 16-byte chunk
+        const half4 lo = lds_read_tr16(eh + mir_off(r, col >> 3) + off);
+        const half4 hi4 = lds_read_tr16(eh + mir_off(r + 4, col >> 3) + off);
+        const half8 h = __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+        const int orow = gcol0 + 16 * cb + si, ocol = grow0 + 8 * rg;
+        const int hi = dtile ? orow - ocol : 8;           // strictly below the diagonal
+        store_h8_range(reinterpret_cast<_Float16 *>(Sym) + size_t(orow) * d.Pp + ocol, h, 0, hi);
+      }
+      __builtin_amdgcn_wave_barrier();
+    } else if (mirror) {
       // transpose: output row = this tile's column, 8 consecutive source rows
 #pragma unroll
       for (int t = 0; t < NTASK; ++t) {
