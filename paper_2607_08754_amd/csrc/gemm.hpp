@@ -458,6 +458,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+  // fp16 Gram: the MFMA operands are swapped (the B-operand fragment first),
+  // so that each lane's accumulator holds 4 consecutive output columns of one
+  // row: acc[i][j][4 g + q] = C[row lr of 32-row block i][column
+  // 32 j + 8 g + 4 lk + q] of the wave tile, as in the persistent update
+  // kernel. (The poly product measured slower this way: its b A term then
+  // needs twice as many, 8-byte, loads of A.)
+  constexpr bool kSwap = sizeof(T) == 2 && MODE == kGram && WTN == 64;
   // fragments of k-step s + 1 are read from LDS while the MFMAs of k-step s run
   auto compute = [&](int buf) {
     const char *sA = smem + buf * S::kStage;
@@ -491,7 +498,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) Mfma<T>::mma(acc[i][j], fa[s & 1][i], fb[s & 1][j]);
+        for (int j = 0; j < FN; ++j) {
+          if constexpr (kSwap)
+            Mfma<T>::mma(acc[i][j], fb[s & 1][j], fa[s & 1][i]);
+          else
+            Mfma<T>::mma(acc[i][j], fa[s & 1][i], fb[s & 1][j]);
+        }
     }
   };
 
@@ -550,6 +562,73 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs args) {
   const bool mirror = (MODE == kGram || MODE == kPoly) && !part;
   const bool dtile = mirror && tile.tm == tile.tn;
   double tsum = 0.0;
+
+  if constexpr (kSwap) {
+    // Per 32-row block: the results (scaled, rounded to fp16 once) go to the
+    // wave's fp16 block with 8-byte writes; 16-byte reads give
+    // 8 consecutive columns for the stores, 8 rows of 128 bytes per
+    // instruction; the mirror transposes the same block with transposing
+    // reads. Gram parts store their fp32 partial straight from the
+    // accumulators.
+    constexpr int NT16 = 32 * 8 / 64;               // 16-byte pieces per lane and block
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int grow0 = m0 + wm * WTM + i * 32, gcol0 = n0 + wn * WTN;
+      if (part) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            float4v f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) f[q] = acc[i][j][4 * g + q];
+            *reinterpret_cast<float4v *>(args.gpart + size_t(tile.slot) * (BM * BN) +
+                                         size_t(grow0 - m0 + lr) * BN + (gcol0 - n0) + 32 * j + 8 * g + 4 * lk) = f;
+          }
+        continue;
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          half4 h;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) h[q] = _Float16(acc[i][j][4 * g + q] * alpha);
+          *reinterpret_cast<half4 *>(eh + mir_off(lr, 4 * j + g) + 8 * lk) = h;
+        }
+      // the block is the wave's own and one wave's LDS operations are
+      // performed in order: a wave-level barrier (no reordering) suffices
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int t = 0; t < NT16; ++t) {
+        const int task = lane + 64 * t, row = task >> 3, cg = task & 7;
+        const half8 h = *reinterpret_cast<const half8 *>(eh + mir_off(row, cg));
+        const int grow = grow0 + row, gcol = gcol0 + 8 * cg;
+        store_h8_range(reinterpret_cast<_Float16 *>(Sym) + size_t(grow) * d.Pp + gcol, h, dtile ? grow - gcol : 0, 8);
+      }
+      if (mirror) {
+        // transpose: each 16-lane group takes 16 columns x 8 rows; two
+        // transposing reads (rows 0-3, 4-7 of the group) leave lane s with
+        // column 16 cb + s, rows 8 rg .. 8 rg + 7: one 16-byte row piece of
+        // the mirror tile
+#pragma unroll
+        for (int t = 0; t < NT16; ++t) {
+          const int q = (lane >> 4) + 4 * t, rg = q & 3, cb = q >> 2, si = lane & 15;
+          const int col = 16 * cb + 4 * (si & 3);          // this lane's 4-column piece
+          const int r = 8 * rg + (si >> 2);
+          const int off = (col & 7) * 2;                   // byte within the 16-byte chunk
+          const half4 lo = lds_read_tr16(eh + mir_off(r, col >> 3) + off);
+          const half4 hi4 = lds_read_tr16(eh + mir_off(r + 4, col >> 3) + off);
+          const half8 h = __builtin_shufflevector(lo, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+          const int orow = gcol0 + 16 * cb + si, ocol = grow0 + 8 * rg;
+          const int hi = dtile ? orow - ocol : 8;         // strictly below the diagonal
+          store_h8_range(reinterpret_cast<_Float16 *>(Sym) + size_t(orow) * d.Pp + ocol, h, 0, hi);
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    return;
+  }
 
   // Poly: the A values of the b A term; Last: the X_0' values of the trace.
   // Loaded one 32-row block ahead (two register buffers). Task t of a lane:
