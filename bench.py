@@ -280,10 +280,18 @@ def main():
         n = args.calibrate_copy << 20
         src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
         dst = torch.empty_like(src)
+        ms = []
         for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
             dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "repeats": 3}), flush=True)
+            e1.record()
+            e1.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        best = min(ms)
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "repeats": 3,
+                          "ms": [round(m, 4) for m in ms],
+                          "tb_per_s_read_plus_write": round(2 * n / (best * 1e-3) / 1e12, 3)}), flush=True)
         return
 
     cfg = CONFIGS[args.config]
