@@ -1094,7 +1094,8 @@ __global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int q = lane + 64 * t, row = q >> 3, ch = q & 7;
-        x0v[i & 1][t] = *reinterpret_cast<const half8 *>(c.X0 + size_t(row_w + i * 32 + row) * c.ldx + col_w + 8 * ch);
+        x0v[i & 1][t] = __builtin_nontemporal_load(
+            reinterpret_cast<const half8 *>(c.X0 + size_t(row_w + i * 32 + row) * c.ldx + col_w + 8 * ch));
       }
     }
   };
