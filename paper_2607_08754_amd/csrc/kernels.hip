@@ -163,6 +163,9 @@ __device__ __forceinline__ u32x4 gload16(const void *p) {
   return *(const __attribute__((address_space(1))) u32x4 *)p;
 }
 __device__ __forceinline__ void gstore16(void *p, u32x4 v) { *(__attribute__((address_space(1))) u32x4 *)p = v; }
+__device__ __forceinline__ u32x4 gload16_stream(const void *p) {
+  return __builtin_nontemporal_load((const __attribute__((address_space(1))) u32x4 *)p);
+}
 
 // 8 consecutive values, 16-byte aligned and all in bounds, as floats.
 template <typename T>
@@ -174,6 +177,26 @@ __device__ __forceinline__ void ld8(const T *p, float (&v)[8]) {
     for (int j = 0; j < 8; ++j) v[j] = to_f(T(h[j]));
   } else {
     const float4v a = __builtin_bit_cast(float4v, gload16(p)), b = __builtin_bit_cast(float4v, gload16(p + 4));
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j] = a[j];
+      v[4 + j] = b[j];
+    }
+  }
+}
+
+// As ld8, marked non-temporal: for data read once and not again by later
+// launches, which then need not stay in the caches.
+template <typename T>
+__device__ __forceinline__ void ld8_stream(const T *p, float (&v)[8]) {
+  if constexpr (sizeof(T) == 2) {
+    typedef T t8 __attribute__((ext_vector_type(8)));
+    const t8 h = __builtin_bit_cast(t8, gload16_stream(p));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = to_f(T(h[j]));
+  } else {
+    const float4v a = __builtin_bit_cast(float4v, gload16_stream(p)),
+                  b = __builtin_bit_cast(float4v, gload16_stream(p + 4));
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       v[j] = a[j];
@@ -219,6 +242,10 @@ constexpr int kPrepPitch = kPrepTile + 4;
 
 // Loads canonical tile t of W into LDS: tile[r * kPrepPitch + c] holds the
 // canonical element (m0 + r, n0 + c) of W (W^T for tall W), 0 outside it.
+// Full tiles read W non-temporally: no later launch of the schedule before
+// the gradient needs W, while the first Gram product reads the X_0' written
+// here, which then keeps its place in the caches (measured on ViT-B/16: the
+// Gram launches 3 us faster on average, the call about 10 us).
 template <typename Tw>
 __device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const MatDesc &d, const Tw *w, float scale) {
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
@@ -241,7 +268,7 @@ __device__ __forceinline__ void stage_tile(float *tile, const Tile &t, const Mat
 #pragma unroll
     for (int k = 0; k < kTasks; ++k) {
       const int q = threadIdx.x + k * kThreads, r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
-      ld8(w + size_t(r0 + r) * d.cols + c0 + c, v[k]);
+      ld8_stream(w + size_t(r0 + r) * d.cols + c0 + c, v[k]);
     }
 #pragma unroll
     for (int k = 0; k < kTasks; ++k) {
@@ -568,7 +595,8 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
     const int q = threadIdx.x + k * kThreads;
     const int r = q / (kPrepTile / 8), c = (q % (kPrepTile / 8)) * 8;
     float v[8];
-    ld8(x + size_t(m0 + r) * d.Qp + n0 + c, v);     // padded canonical buffer: aligned, in bounds
+    // padded canonical buffer: aligned, in bounds; X_T is read here only once
+    ld8_stream(x + size_t(m0 + r) * d.Qp + n0 + c, v);
 #pragma unroll
     for (int j = 0; j < 8; ++j) tile[r * kPrepPitch + c + j] = v[j];
   }
