@@ -1158,7 +1158,12 @@ __global__ __launch_bounds__(512) void k_upd256(GemmArgs args) {
         const int c = lane + 64 * t, row = c >> 3, ch = c & 7;
         const half8 h = *reinterpret_cast<const half8 *>(ep + epi_off(row, ch));
         const size_t o = size_t(row_w + i * 32 + row) * cur.ldx + col_w + 8 * ch;
-        if (MODE == kUpdate || args.write_x) __builtin_nontemporal_store(h, reinterpret_cast<half8 *>(cur.Xn + o));
+        // the iterate of a step is streamed out (the next launch reads it,
+        // and its lines would evict operand panels this launch still reads);
+        // X_T, read by the gradient kernel two short launches later, is
+        // stored normally (measured faster)
+        if constexpr (MODE == kUpdate) __builtin_nontemporal_store(h, reinterpret_cast<half8 *>(cur.Xn + o));
+        else if (args.write_x) *reinterpret_cast<half8 *>(cur.Xn + o) = h;
         if constexpr (MODE == kLast) tsum += double(trace8(h, x0v[i & 1][t]));   // P as stored times X_0'
       }
       if (i + 2 < U::FM) x0load(cur, i + 2);
