@@ -21,7 +21,8 @@
 //                        Frobenius norms")
 //   k_finalize values L_i and gradient factors, one block per matrix
 //              (Sec. 3 definitions; Eq. SLORR_grads; Listing 1)
-//   k_setsum   the set total in index order (Sec. 3, L summed over the set)
+//   k_setsum   the set total in index order (Sec. 3, L summed over the set),
+//              when no gradient launch follows (k_grad's first block otherwise)
 //   k_gram_reduce  A = X X^T from split-K partial tiles (sets with few, long
 //              Gram tiles), fixed summation order
 //   k_grad     grad = g (s1 P - s2 W)  (Hoyer) or g P (nuclear) from the last
@@ -452,14 +453,15 @@ __global__ __launch_bounds__(64) void k_finalize(const MatDesc *__restrict__ mat
   }
 }
 
-// The set total sum_i L_i, added in index order (fp64): the values are
-// staged in LDS a chunk at a time and one thread adds them.
-__global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
-                                                 const CallParams *__restrict__ call, int n) {
-  __shared__ double v[1024];
+// The set total sum_i L_i, added in index order (fp64) by one block of NTH
+// threads: the values are staged in LDS (v, NTH entries) a chunk at a time
+// and one thread adds them. The result does not depend on NTH.
+template <int NTH>
+__device__ __forceinline__ void set_total(const Scalars *__restrict__ sc, const CallParams *__restrict__ call,
+                                          int n, double *v) {
   double tot = 0.0;
-  for (int base = 0; base < n; base += 1024) {
-    const int m = min(1024, n - base);
+  for (int base = 0; base < n; base += NTH) {
+    const int m = min(NTH, n - base);
     if (int(threadIdx.x) < m) v[threadIdx.x] = sc[base + threadIdx.x].value;
     __syncthreads();
     if (threadIdx.x == 0)
@@ -467,6 +469,14 @@ __global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
     __syncthreads();
   }
   if (threadIdx.x == 0) call->out_vals[n] = float(tot);
+}
+
+// The set total on its own (calls that compute no gradient; otherwise the
+// gradient launch's first block writes it).
+__global__ __launch_bounds__(1024) void k_setsum(const Scalars *__restrict__ sc,
+                                                 const CallParams *__restrict__ call, int n) {
+  __shared__ double v[1024];
+  set_total<1024>(sc, call, n, v);
 }
 
 // Split-K Gram: A tile = alpha * (sum of its fp32 partials, in part order),
@@ -550,9 +560,13 @@ __global__ __launch_bounds__(kThreads) void k_grad(const Tile *__restrict__ tile
                                                    const Scalars *__restrict__ sc,
                                                    const CallParams *__restrict__ call,
                                                    const char *__restrict__ ws, float inv_sx,
-                                                   int accumulate) {
+                                                   int accumulate, int set_sum, int n) {
 #pragma clang fp contract(off)
   __shared__ __attribute__((aligned(16))) float tile[kPrepTile * kPrepPitch];
+  if (set_sum && blockIdx.x == 0) {     // the set total (the values are final)
+    __shared__ double v[kThreads];
+    set_total<kThreads>(sc, call, n, v);
+  }
   const Tile t = tiles[blockIdx.x];
   const MatDesc d = mats[t.mat];
   const int m0 = t.tm * kPrepTile, n0 = t.tn * kPrepTile;
@@ -750,9 +764,11 @@ void launch_grad(const Plan &p, const Launch &l, hipStream_t s, const EvPair *ev
   const float inv_sx = 1.0f / (sizeof(Tx) == 2 ? kScaleX16 : 1.0f);
   const int acc = (p.flags & SLORR_ACCUMULATE) ? 1 : 0;
   if (p.grad_dtype == SLORR_BF16)
-    go(k_grad<Tw, Tx, bf16_t>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc);
+    go(k_grad<Tw, Tx, bf16_t>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc,
+       l.set_sum, p.n);
   else
-    go(k_grad<Tw, Tx, float>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc);
+    go(k_grad<Tw, Tx, float>, dim3(l.grid), dim3(kThreads), s, ev, tiles, mats, dyn, sc, call, ws, inv_sx, acc,
+       l.set_sum, p.n);
 }
 
 template <typename Tw, typename Tx>

@@ -454,16 +454,20 @@ void build_plan(Plan &p) {
     }
   }
   if (p.n > 0) p.launches.push_back(plain(Op::Finalize, p.n));
-  p.launches.push_back(plain(Op::SetSum, 1));
   // The gradient, once s1 and s2 are known, by the gradient kernel from the
   // stored X_T. A deferred gradient runs the same launch later, from the X_T
-  // and the factors the forward left in the workspace.
+  // and the factors the forward left in the workspace. The set total (the
+  // values added in index order) is written by the gradient launch's first
+  // block when the call computes the gradient, else by a launch of its own.
+  const bool grad_now = !(p.flags & (SLORR_VALUES_ONLY | SLORR_DEFER_GRAD)) && p.prep.count;
+  if (!grad_now) p.launches.push_back(plain(Op::SetSum, 1));
   p.grad_launches.clear();
   if (!(p.flags & SLORR_VALUES_ONLY)) {
     const size_t first = p.launches.size();
     if (p.prep.count) p.launches.push_back(plain(Op::Grad, p.prep.count, p.prep.first));
     p.grad_launches.assign(p.launches.begin() + first, p.launches.end());
     if (p.flags & SLORR_DEFER_GRAD) p.launches.resize(first);
+    else if (grad_now) p.launches.back().set_sum = 1;
   }
 
   // MFMA work the launches execute (padded, symmetric tiles counted once)

@@ -46,6 +46,7 @@ struct Launch {
   int32_t use_a;       // update operand is A (cubic step) instead of B
   int32_t fold;        // update: a_t I already folded into B (no a X term)
   int32_t kap;         // first step: coefficients scaled per matrix by powers of kappa
+  int32_t set_sum;     // gradient launch: its first block also writes the set total
   float alpha, beta, gamma;  // epilogue coefficients
 };
 

@@ -375,13 +375,17 @@ void check(Plan &p) {
       EXPECT(op_at(k) == Op::Finalize && L[k].grid == p.n, "finalize");
       ++k;
     }
-    EXPECT(op_at(k) == Op::SetSum, "set sum at launch %zu", k);
-    ++k;
     const bool grad = !(p.flags & SLORR_VALUES_ONLY) && !live.empty();
-    if (grad && !(p.flags & SLORR_DEFER_GRAD)) {
-      EXPECT(op_at(k) == Op::Grad && L[k].grid == p.prep.count, "gradient launch");
+    const bool grad_now = grad && !(p.flags & SLORR_DEFER_GRAD);
+    if (grad_now) {                    // its first block writes the set total
+      EXPECT(op_at(k) == Op::Grad && L[k].grid == p.prep.count && L[k].set_sum == 1, "gradient launch");
+      ++k;
+    } else {
+      EXPECT(op_at(k) == Op::SetSum, "set sum at launch %zu", k);
       ++k;
     }
+    for (const Launch &l : L) EXPECT(l.set_sum == (grad_now && l.op == Op::Grad ? 1 : 0), "set_sum flag");
+    for (const Launch &l : p.grad_launches) EXPECT(l.set_sum == 0, "deferred gradient writes no set total");
     EXPECT(k == L.size(), "%zu launches, %zu checked", L.size(), k);
     EXPECT(p.grad_launches.size() == (grad ? 1u : 0u), "%zu gradient launches", p.grad_launches.size());
   }
