@@ -129,6 +129,10 @@ def test_deferred_gradient_equals_one_call_path():
     # values-only route
     v2 = reg.values()
     assert torch.equal(v2[: len(shapes)], L.detach())
+    # the set total: written by the gradient launch in the one-call plan and
+    # by a launch of its own in the values-only plan, the same sum in the same order
+    n = len(shapes)
+    assert torch.equal(vals[n], v2[n])
 
 
 def test_backward_after_another_forward_raises():
